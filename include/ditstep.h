@@ -1,0 +1,234 @@
+/*
+ * ditstep.h -- C ABI of the MI355X (gfx950) K-seed DiT denoise-step library.
+ *
+ * One denoising step of a diffusion transformer, run for the K seeds of a
+ * prompt group (the rollout / seed-exploration unit of GRPO-style DiT RL
+ * post-training: K samples per prompt from distinct seeds, Spotlight paper
+ * section 2.1 and Fig. "fig:grpo"; every step is one forward pass of the DiT
+ * backbone, section 2.1), followed by the flow-matching sampler update
+ * (FlowGRPO backbone, section 5) and the per-prompt-group reward statistics
+ * with seed ordering used for top/bottom seed selection (sigma_g of section
+ * 4.3.2; top-k/bottom-k selection of section 5 "Dynamic Exploration").
+ *
+ * Conventions for every entry point
+ *   - Tensors are caller-owned DEVICE pointers (hipMalloc / torch on the GPU)
+ *     unless stated otherwise; the library never frees them and performs no
+ *     device allocation on the hot path. Scratch memory comes from a
+ *     caller-provided workspace whose size the *_workspace_bytes() calls give.
+ *   - Every call is asynchronous on `stream` (a hipStream_t; NULL = the null
+ *     stream), except group_reward_stats, which synchronises `stream` once
+ *     to check its small input for NaN.
+ *   - Arguments are validated before any launch; on any error nothing is
+ *     written, the status says why and dit_last_error_message() (per host
+ *     thread) gives detail. Launch failures return DIT_ERR_HIP.
+ *   - Layouts are row-major with the last index contiguous. Linear weights
+ *     are stored [out][in] (both GEMM operands K-contiguous); biases [out].
+ *   - Element types: DIT_BF16 = bfloat16 storage with fp32 accumulation and
+ *     fp32 epilogue math; DIT_F32 = fp32 throughout. temb, the latent, the
+ *     velocity, noise and rewards are always fp32.
+ *   - Thread safety: no mutable global state besides the per-thread error
+ *     text; calls on different streams with disjoint buffers may overlap.
+ */
+#ifndef DITSTEP_H
+#define DITSTEP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DIT_ABI_VERSION 1
+
+typedef enum {
+  DIT_OK = 0,
+  DIT_ERR_INVALID_ARG = 1,  /* NULL required pointer, negative size, k_select > n, ... */
+  DIT_ERR_SHAPE = 2,        /* inconsistent shape (hidden != heads*head_dim, n_img != grid_h*grid_w, ...) */
+  DIT_ERR_DOMAIN = 3,       /* flow_step: noise_level > 0 with t outside (0,1), or t_next > t, ... */
+  DIT_ERR_NAN = 4,          /* group_reward_stats: a reward is NaN or infinite */
+  DIT_ERR_UNSUPPORTED = 5,  /* valid but not implemented (head_dim not 64/128, hidden > 4096, ...) */
+  DIT_ERR_HIP = 6,          /* a HIP runtime call or kernel launch failed */
+  DIT_ERR_WORKSPACE = 7     /* workspace NULL, misaligned (256 B) or smaller than required */
+} dit_status;
+
+typedef enum { DIT_F32 = 0, DIT_BF16 = 1 } dit_dtype;
+
+typedef void* dit_stream; /* hipStream_t */
+
+/* Shape of one dual-stream MMDiT block (image stream + text stream, joint
+ * attention). Sequence order inside the block is [text ; image]. */
+typedef struct {
+  int32_t hidden;      /* D = heads * head_dim, multiple of 64, <= 4096 */
+  int32_t heads;       /* H */
+  int32_t head_dim;    /* d, 64 or 128 */
+  int32_t mlp_hidden;  /* F (4*D in the configurations used), multiple of 64 */
+  int32_t n_img;       /* N_i image tokens = grid_h * grid_w */
+  int32_t n_txt;       /* N_t text tokens (>= 0) */
+  int32_t grid_h;      /* latent token grid (rows) */
+  int32_t grid_w;      /* latent token grid (columns) */
+  int32_t rope;        /* nonzero: 2D axial RoPE on image-token q and k */
+  float ln_eps;        /* LayerNorm epsilon (1e-6) */
+  float rope_theta;    /* RoPE base (1e4) */
+  int32_t dtype;       /* dit_dtype of weights and activations */
+} dit_block_config;
+
+/* Weights of one block; index 0 = image stream, 1 = text stream. Element
+ * type = config dtype. Shapes ([out][in]):
+ *   mod_w [6D][D], mod_b [6D]   adaLN modulation, chunks in the order
+ *                               shift1, scale1, gate1, shift2, scale2, gate2
+ *   qkv_w [3D][D], qkv_b [3D]   rows [0,D) -> q, [D,2D) -> k, [2D,3D) -> v;
+ *                               head j owns columns [j*d, (j+1)*d) of each
+ *   out_w [D][D],  out_b [D]
+ *   mlp1_w [F][D], mlp1_b [F]
+ *   mlp2_w [D][F], mlp2_b [D] */
+typedef struct {
+  const void* mod_w[2];
+  const void* mod_b[2];
+  const void* qkv_w[2];
+  const void* qkv_b[2];
+  const void* out_w[2];
+  const void* out_b[2];
+  const void* mlp1_w[2];
+  const void* mlp1_b[2];
+  const void* mlp2_w[2];
+  const void* mlp2_b[2];
+} dit_block_weights;
+
+/* Weights around the block stack for a full step (element type = config dtype):
+ *   t1_w [D][256], t1_b [D], t2_w [D][D], t2_b [D]   timestep MLP
+ *   in_w [D][C],   in_b [D]                          patch embedding, C = latent_dim
+ *   fmod_w [2D][D], fmod_b [2D]                      final modulation (shift_f, scale_f)
+ *   fout_w [C][D], fout_b [C]                        velocity head */
+typedef struct {
+  const void* t1_w;
+  const void* t1_b;
+  const void* t2_w;
+  const void* t2_b;
+  const void* in_w;
+  const void* in_b;
+  const void* fmod_w;
+  const void* fmod_b;
+  const void* fout_w;
+  const void* fout_b;
+} dit_step_weights;
+
+/* ------------------------------------------------------------------ */
+/* library                                                              */
+/* ------------------------------------------------------------------ */
+int32_t dit_abi_version(void);
+const char* dit_status_string(dit_status s);
+/* Detail of the last non-OK status returned on the calling host thread. */
+const char* dit_last_error_message(void);
+
+/* ------------------------------------------------------------------ */
+/* one MMDiT block (the DiT forward pass is a stack of these)           */
+/* ------------------------------------------------------------------ */
+/* Bytes of workspace dit_block_forward / dit_block_mlp need for `batch`. */
+size_t dit_block_workspace_bytes(const dit_block_config* cfg, int32_t batch);
+
+/* One dual-stream MMDiT block, in place on both residual streams.
+ *   temb  [B][D] fp32        per-sample conditioning vector
+ *   x_img [B][N_i][D]        image residual stream (in/out), config dtype
+ *   x_txt [B][N_t][D]        text residual stream (in/out), config dtype
+ * Per stream s: (shift1..gate2) = W_mod SiLU(temb) + b_mod;
+ *   h = LN(x)(1+scale1)+shift1; q,k,v = W_qkv h + b_qkv; RoPE on image q,k;
+ *   o = softmax(q k^T / sqrt(d)) v over all S = N_t + N_i tokens, per head;
+ *   x += gate1 * (W_o o + b_o); h2 = LN(x)(1+scale2)+shift2;
+ *   x += gate2 * (W_2 GELU_tanh(W_1 h2 + b_1) + b_2).
+ * workspace: device, 256-byte aligned, >= dit_block_workspace_bytes(). */
+dit_status dit_block_forward(const dit_block_config* cfg, const dit_block_weights* w, int32_t batch,
+                             const float* temb, void* x_img, void* x_txt,
+                             void* workspace, size_t workspace_bytes, dit_stream stream);
+
+/* Only the MLP half of dit_block_forward (modulation, then
+ * x += gate2 * MLP(LN(x)(1+scale2)+shift2) on both streams). This is the
+ * per-token part a sequence-parallel rank runs on its own token slice. */
+dit_status dit_block_mlp(const dit_block_config* cfg, const dit_block_weights* w, int32_t batch,
+                         const float* temb, void* x_img, void* x_txt,
+                         void* workspace, size_t workspace_bytes, dit_stream stream);
+
+/* Joint non-causal multi-head attention, o = softmax(q k^T * scale) v per
+ * (sample, head), every query attending to all `seq` keys.
+ * q, k, v: element (b, s, h, e) at base + b*qkv_stride_b + s*qkv_stride_s +
+ *   h*qkv_stride_h + e (strides in ELEMENTS, e contiguous), so q/k/v may be
+ *   slices of one packed [B][S][3][H][d] buffer.
+ * o: element (b, s, h, e) at o + b*o_stride_b + s*o_stride_s + h*o_stride_h + e.
+ * head_dim: 64 or 128. scale: usually 1/sqrt(head_dim). dtype: DIT_BF16
+ * (bf16 MFMA, fp32 softmax) or DIT_F32. Pointers and strides must keep
+ * 16-byte alignment of every (b, s, h) row. */
+dit_status joint_attention(const void* q, const void* k, const void* v, void* o,
+                           int32_t batch, int32_t heads, int32_t seq, int32_t head_dim,
+                           int64_t qkv_stride_b, int64_t qkv_stride_s, int64_t qkv_stride_h,
+                           int64_t o_stride_b, int64_t o_stride_s, int64_t o_stride_h,
+                           float scale, int32_t dtype, dit_stream stream);
+
+/* ------------------------------------------------------------------ */
+/* sampler and reward statistics                                        */
+/* ------------------------------------------------------------------ */
+/* One flow-matching sampler step on n fp32 elements, in place on x.
+ * h = t_next - t (<= 0; noise at t = 1, data at t = 0).
+ *   noise_level == 0: x' = x + h v                              (Euler ODE)
+ *   noise_level  > 0: sigma = a sqrt(t/(1-t)),
+ *     x' = x + h (v + sigma^2/(2t) (x + (1-t) v)) + sigma sqrt(-h) noise  (SDE)
+ * noise may be NULL iff noise_level == 0. Errors: DIT_ERR_DOMAIN if
+ * noise_level < 0, t_next > t, t or t_next not finite, or noise_level > 0
+ * with t outside (0,1) or t_next < 0. n == 0 is a no-op. */
+dit_status flow_step(float* x, const float* v, const float* noise, int64_t n,
+                     float t, float t_next, float noise_level, dit_stream stream);
+
+/* Per prompt-group statistics over rewards [G][n] fp32 (row g = the n seeds
+ * of prompt group g):
+ *   mean[g] = sum_j r / n; std[g] = sqrt(sum_j (r - mean)^2 / n) (population);
+ *   adv[g][j] = (r - mean) / (std + adv_eps);
+ *   order[g][:] = seed indices by descending reward, ties by ascending index;
+ *   selected[g][:] = order[g][0 : ceil(k/2)] then order[g][n - floor(k/2) : n].
+ * Outputs (device): mean, std [G] fp32; adv [G][n] fp32; order [G][n] int32;
+ * selected [G][k_select] int32. Any output may be NULL (skipped).
+ * 1 <= n <= 4096; 0 <= k_select <= n. A NaN/Inf reward returns DIT_ERR_NAN
+ * and writes nothing (the call synchronises `stream` to check). */
+dit_status group_reward_stats(const float* rewards, int32_t groups, int32_t n, float adv_eps,
+                              int32_t k_select, float* mean, float* std, float* adv,
+                              int32_t* order, int32_t* selected, dit_stream stream);
+
+/* ------------------------------------------------------------------ */
+/* full denoise step                                                    */
+/* ------------------------------------------------------------------ */
+/* temb [B][D] fp32 = W_2 SiLU(W_1 e(t) + b_1) + b_2 with
+ * e(t) = [cos(1000 t f_j) ; sin(1000 t f_j)], f_j = 10000^(-j/128), j < 128.
+ * t: device [B] fp32. */
+dit_status dit_timestep_embed(const dit_block_config* cfg, const dit_step_weights* w, int32_t batch,
+                              const float* t, float* temb, void* workspace, size_t workspace_bytes,
+                              dit_stream stream);
+
+/* x_img [B][N_i][D] (config dtype) = W_in latent + b_in; latent [B][N_i][C] fp32. */
+dit_status dit_patch_embed(const dit_block_config* cfg, const dit_step_weights* w, int32_t batch,
+                           int32_t latent_dim, const float* latent, void* x_img,
+                           void* workspace, size_t workspace_bytes, dit_stream stream);
+
+/* v [B][N_i][C] fp32 = W_out (LN(x_img)(1+scale_f)+shift_f) + b_out,
+ * (shift_f, scale_f) = W_f SiLU(temb) + b_f. */
+dit_status dit_final_layer(const dit_block_config* cfg, const dit_step_weights* w, int32_t batch,
+                           int32_t latent_dim, const float* temb, const void* x_img, float* v,
+                           void* workspace, size_t workspace_bytes, dit_stream stream);
+
+/* Workspace for dit_denoise_step (includes the residual streams). */
+size_t dit_denoise_workspace_bytes(const dit_block_config* cfg, int32_t batch, int32_t latent_dim);
+
+/* One K-seed denoise step: temb(t) -> patch embedding -> n_blocks blocks ->
+ * velocity -> flow_step(t -> t_next, noise_level) in place on latent.
+ *   t, t_next  the step's timestep and the next one (all K seeds share t)
+ *   latent  [B][N_i][C] fp32 (in/out); x_txt [B][N_t][D] text hidden input
+ *           (config dtype, read only); noise [B][N_i][C] fp32 (NULL iff
+ *           noise_level == 0); v_out [B][N_i][C] fp32 velocity (may be NULL).
+ *   blocks  host array of n_blocks weight sets. */
+dit_status dit_denoise_step(const dit_block_config* cfg, const dit_step_weights* sw,
+                            const dit_block_weights* blocks, int32_t n_blocks, int32_t batch,
+                            int32_t latent_dim, float t, float t_next,
+                            float noise_level, float* latent, const void* x_txt, const float* noise,
+                            float* v_out, void* workspace, size_t workspace_bytes, dit_stream stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DITSTEP_H */

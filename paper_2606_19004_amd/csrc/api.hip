@@ -1,0 +1,609 @@
+// C ABI of the denoise-step library: argument validation, workspace layout and
+// the launch sequence of each entry point (see include/ditstep.h).
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+#include <vector>
+
+#include "../../include/ditstep.h"
+#include "internal.h"
+
+using namespace dit;
+
+namespace {
+
+thread_local std::string g_err;
+
+dit_status fail(dit_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+#define HIP_TRY(expr)                                                                         \
+  do {                                                                                        \
+    hipError_t e_ = (expr);                                                                   \
+    if (e_ != hipSuccess) return fail(DIT_ERR_HIP, "%s failed: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+inline size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
+inline bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+inline size_t esize(int32_t dtype) { return dtype == DIT_BF16 ? 2 : 4; }
+inline hipStream_t hs(dit_stream s) { return (hipStream_t)s; }
+
+dit_status check_config(const dit_block_config* c) {
+  if (!c) return fail(DIT_ERR_INVALID_ARG, "config is NULL");
+  if (c->dtype != DIT_F32 && c->dtype != DIT_BF16) return fail(DIT_ERR_INVALID_ARG, "dtype %d invalid", c->dtype);
+  if (c->hidden <= 0 || c->heads <= 0 || c->head_dim <= 0 || c->mlp_hidden <= 0)
+    return fail(DIT_ERR_SHAPE, "hidden/heads/head_dim/mlp_hidden must be positive");
+  if (c->hidden != c->heads * c->head_dim)
+    return fail(DIT_ERR_SHAPE, "hidden %d != heads %d * head_dim %d", c->hidden, c->heads, c->head_dim);
+  if (c->head_dim != 64 && c->head_dim != 128) return fail(DIT_ERR_UNSUPPORTED, "head_dim %d (64 or 128)", c->head_dim);
+  if (c->hidden % 64 || c->mlp_hidden % 64) return fail(DIT_ERR_UNSUPPORTED, "hidden and mlp_hidden must be multiples of 64");
+  if (c->hidden > 4096) return fail(DIT_ERR_UNSUPPORTED, "hidden %d > 4096", c->hidden);
+  if (c->grid_h <= 0 || c->grid_w <= 0 || c->n_img != c->grid_h * c->grid_w)
+    return fail(DIT_ERR_SHAPE, "n_img %d != grid_h %d * grid_w %d", c->n_img, c->grid_h, c->grid_w);
+  if (c->n_txt < 0) return fail(DIT_ERR_SHAPE, "n_txt %d < 0", c->n_txt);
+  if (!(c->ln_eps > 0.f) || !std::isfinite(c->ln_eps)) return fail(DIT_ERR_INVALID_ARG, "ln_eps must be positive");
+  if (c->rope && (!(c->rope_theta > 0.f) || !std::isfinite(c->rope_theta)))
+    return fail(DIT_ERR_INVALID_ARG, "rope_theta must be positive");
+  return DIT_OK;
+}
+
+dit_status check_ws(void* ws, size_t have, size_t need) {
+  if (need == 0) return DIT_OK;
+  if (!ws) return fail(DIT_ERR_WORKSPACE, "workspace is NULL (%zu bytes needed)", need);
+  if ((uintptr_t)ws & 255) return fail(DIT_ERR_WORKSPACE, "workspace not 256-byte aligned");
+  if (have < need) return fail(DIT_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", have, need);
+  return DIT_OK;
+}
+
+// offsets into the block workspace
+struct BlockWs {
+  size_t mod, silu, rope, h, qkv, u, total;
+};
+BlockWs block_layout(const dit_block_config* c, int64_t B) {
+  BlockWs w;
+  size_t es = esize(c->dtype);
+  size_t S = (size_t)c->n_img + c->n_txt, D = c->hidden, F = c->mlp_hidden;
+  size_t npos = std::max(c->grid_h, c->grid_w);
+  size_t off = 0;
+  w.mod = off;  off += al256(2 * B * 6 * D * 4);
+  w.silu = off; off += al256(B * D * 4);
+  w.rope = off; off += al256(npos * (c->head_dim / 4) * 2 * 4);
+  w.h = off;    off += al256(B * S * D * es);
+  w.qkv = off;  off += al256(B * S * 3 * D * es);
+  w.u = off;    off += al256(B * S * F * es);
+  w.total = off;
+  return w;
+}
+
+dit_status check_block_args(const dit_block_config* c, const dit_block_weights* w, int32_t batch,
+                            const float* temb, void* x_img, void* x_txt) {
+  dit_status st = check_config(c);
+  if (st) return st;
+  if (!w) return fail(DIT_ERR_INVALID_ARG, "weights is NULL");
+  if (batch < 0) return fail(DIT_ERR_INVALID_ARG, "batch %d < 0", batch);
+  if (batch == 0) return DIT_OK;
+  if (!temb || !x_img || (c->n_txt > 0 && !x_txt)) return fail(DIT_ERR_INVALID_ARG, "temb/x_img/x_txt NULL");
+  if (!aligned16(temb) || !aligned16(x_img) || (x_txt && !aligned16(x_txt)))
+    return fail(DIT_ERR_INVALID_ARG, "temb/x_img/x_txt must be 16-byte aligned");
+  for (int s = 0; s < 2; s++) {
+    if (!w->mod_w[s] || !w->qkv_w[s] || !w->out_w[s] || !w->mlp1_w[s] || !w->mlp2_w[s])
+      return fail(DIT_ERR_INVALID_ARG, "a weight matrix of stream %d is NULL", s);
+    const void* all[10] = {w->mod_w[s], w->mod_b[s], w->qkv_w[s], w->qkv_b[s], w->out_w[s],
+                           w->out_b[s], w->mlp1_w[s], w->mlp1_b[s], w->mlp2_w[s], w->mlp2_b[s]};
+    for (const void* p : all)
+      if (p && ((uintptr_t)p & 7)) return fail(DIT_ERR_INVALID_ARG, "weights must be 8-byte aligned");
+  }
+  // the MFMA GEMM addresses its A operand with 31-bit byte offsets
+  if (c->dtype == DIT_BF16) {
+    double S = (double)c->n_img + c->n_txt;
+    double big = (double)batch * S * std::max(3 * c->hidden, c->mlp_hidden) * 2.0;
+    if (big >= 2147483648.0) return fail(DIT_ERR_UNSUPPORTED, "activation buffer of %.0f bytes exceeds 2 GiB", big);
+  }
+  return DIT_OK;
+}
+
+// One stream's slice of a joint [B][S][cols] buffer (text rows first).
+RowMap joint_rows(const dit_block_config* c, int stream, int64_t cols) {
+  int64_t S = (int64_t)c->n_img + c->n_txt;
+  if (stream == 0) return RowMap{c->n_img, S * cols, cols, (int64_t)c->n_txt * cols};
+  return RowMap{std::max(c->n_txt, 1), S * cols, cols, 0};
+}
+RowMap stream_rows(int64_t n, int64_t cols) { return RowMap{std::max<int64_t>(n, 1), n * cols, cols, 0}; }
+
+// mod[s][b][6D] = W_mod[s] SiLU(temb[b]) + b_mod[s]
+dit_status run_modulation(const dit_block_config* c, const dit_block_weights* w, int B, const float* temb,
+                          char* ws, const BlockWs& L, hipStream_t s) {
+  const int D = c->hidden;
+  float* silu = (float*)(ws + L.silu);
+  float* mod = (float*)(ws + L.mod);
+  HIP_TRY(silu_f32(temb, silu, (int64_t)B * D, s));
+  GemvArgs g{};
+  for (int st = 0; st < 2; st++) {
+    g.W[st] = w->mod_w[st];
+    g.bias[st] = w->mod_b[st];
+    g.out[st] = mod + (size_t)st * B * 6 * D;
+  }
+  g.out_bstride = 6 * D;
+  g.in = silu;
+  g.in_bstride = D;
+  g.N = 6 * D;
+  g.K = D;
+  g.B = B;
+  g.nstreams = 2;
+  HIP_TRY(gemv(g, c->dtype, s));
+  return DIT_OK;
+}
+
+// h = LN(x)(1+scale)+shift for both streams into the joint [B][S][D] buffer
+dit_status run_ln(const dit_block_config* c, int B, const void* x_img, const void* x_txt, char* ws,
+                  const BlockWs& L, int shift_off, int scale_off, hipStream_t s) {
+  const int D = c->hidden;
+  float* mod = (float*)(ws + L.mod);
+  LnArgs a{};
+  a.x[0] = x_img;
+  a.x[1] = x_txt;
+  a.xmap[0] = stream_rows(c->n_img, D);
+  a.xmap[1] = stream_rows(c->n_txt, D);
+  a.out = ws + L.h;
+  a.omap[0] = joint_rows(c, 0, D);
+  a.omap[1] = joint_rows(c, 1, D);
+  a.mod[0] = mod;
+  a.mod[1] = mod + (size_t)B * 6 * D;
+  a.mod_bstride = 6 * D;
+  a.shift_off = shift_off;
+  a.scale_off = scale_off;
+  a.rows[0] = (int64_t)B * c->n_img;
+  a.rows[1] = (int64_t)B * c->n_txt;
+  a.D = D;
+  a.eps = c->ln_eps;
+  HIP_TRY(ln_modulate(a, c->dtype, s));
+  return DIT_OK;
+}
+
+GemmProblem problem(const void* A, RowMap am, const void* W, const void* bias, void* C, RowMap cm, int M, int N, int K) {
+  GemmProblem p{};
+  p.A = A;
+  p.amap = am;
+  p.W = W;
+  p.bias = bias;
+  p.C = C;
+  p.cmap = cm;
+  p.M = M;
+  p.N = N;
+  p.K = K;
+  return p;
+}
+
+// the MLP half: h2 = LN(x)(1+scale2)+shift2; u = GELU(W1 h2 + b1); x += gate2 (W2 u + b2)
+dit_status run_mlp_half(const dit_block_config* c, const dit_block_weights* w, int B, void* x_img, void* x_txt,
+                        char* ws, const BlockWs& L, hipStream_t s) {
+  const int D = c->hidden, F = c->mlp_hidden;
+  const int rows[2] = {B * c->n_img, B * c->n_txt};
+  void* x[2] = {x_img, x_txt};
+  const int64_t nstream[2] = {c->n_img, c->n_txt};
+  float* mod = (float*)(ws + L.mod);
+  dit_status st = run_ln(c, B, x_img, x_txt, ws, L, 3 * D, 4 * D, s);
+  if (st) return st;
+  GemmPair up{}, down{};
+  up.nprob = down.nprob = 2;
+  for (int i = 0; i < 2; i++) {
+    up.p[i] = problem(ws + L.h, joint_rows(c, i, D), w->mlp1_w[i], w->mlp1_b[i], ws + L.u, joint_rows(c, i, F),
+                      rows[i], F, D);
+    down.p[i] = problem(ws + L.u, joint_rows(c, i, F), w->mlp2_w[i], w->mlp2_b[i], x[i], stream_rows(nstream[i], D),
+                        rows[i], D, F);
+    down.p[i].gate = mod + (size_t)i * B * 6 * D + 5 * D;
+    down.p[i].gate_bstride = 6 * D;
+  }
+  HIP_TRY(gemm(up, EPI_GELU, c->dtype, false, s));
+  HIP_TRY(gemm(down, EPI_RESID, c->dtype, false, s));
+  return DIT_OK;
+}
+
+struct StepWs {
+  size_t temb, ximg, xtxt, v, inner, total;
+};
+
+size_t timestep_ws(const dit_block_config* c, int64_t B) { return al256(B * 256 * 4) + 2 * al256(B * c->hidden * 4); }
+size_t patch_ws(const dit_block_config* c, int64_t B, int C) {
+  return c->dtype == DIT_BF16 ? al256(B * c->n_img * C * 2) : 0;
+}
+size_t final_ws(const dit_block_config* c, int64_t B) {
+  return al256(B * c->hidden * 4) + al256(B * 2 * c->hidden * 4) + al256(B * c->n_img * c->hidden * esize(c->dtype));
+}
+
+StepWs step_layout(const dit_block_config* c, int64_t B, int C) {
+  StepWs w;
+  size_t es = esize(c->dtype);
+  size_t off = 0;
+  w.temb = off; off += al256(B * c->hidden * 4);
+  w.ximg = off; off += al256(B * c->n_img * c->hidden * es);
+  w.xtxt = off; off += al256(B * c->n_txt * c->hidden * es);
+  w.v = off;    off += al256(B * c->n_img * C * 4);
+  w.inner = off;
+  size_t inner = std::max({block_layout(c, B).total, timestep_ws(c, B), patch_ws(c, B, C), final_ws(c, B)});
+  w.total = off + inner;
+  return w;
+}
+
+dit_status check_step_weights(const dit_step_weights* w) {
+  if (!w) return fail(DIT_ERR_INVALID_ARG, "step weights NULL");
+  if (!w->t1_w || !w->t2_w || !w->in_w || !w->fmod_w || !w->fout_w)
+    return fail(DIT_ERR_INVALID_ARG, "a step weight matrix is NULL");
+  return DIT_OK;
+}
+
+dit_status run_timestep(const dit_block_config* c, const dit_step_weights* w, int B, const float* t_dev, float t,
+                        float* temb, char* ws, hipStream_t s) {
+  const int D = c->hidden;
+  float* e = (float*)ws;
+  float* h1 = (float*)(ws + al256((size_t)B * 256 * 4));
+  float* s1 = (float*)(ws + al256((size_t)B * 256 * 4) + al256((size_t)B * D * 4));
+  HIP_TRY(timestep_sinusoid(t_dev, t, e, B, s));
+  GemvArgs g{};
+  g.W[0] = w->t1_w;
+  g.bias[0] = w->t1_b;
+  g.out[0] = h1;
+  g.out_bstride = D;
+  g.in = e;
+  g.in_bstride = 256;
+  g.N = D;
+  g.K = 256;
+  g.B = B;
+  g.nstreams = 1;
+  HIP_TRY(gemv(g, c->dtype, s));
+  HIP_TRY(silu_f32(h1, s1, (int64_t)B * D, s));
+  g.W[0] = w->t2_w;
+  g.bias[0] = w->t2_b;
+  g.out[0] = temb;
+  g.in = s1;
+  g.in_bstride = D;
+  g.K = D;
+  HIP_TRY(gemv(g, c->dtype, s));
+  return DIT_OK;
+}
+
+dit_status run_patch(const dit_block_config* c, const dit_step_weights* w, int B, int C, const float* latent,
+                     void* x_img, char* ws, hipStream_t s) {
+  const int D = c->hidden;
+  const int M = B * c->n_img;
+  const void* A = latent;
+  if (c->dtype == DIT_BF16) {
+    HIP_TRY(cast_f32_to_bf16(latent, (u16*)ws, (int64_t)M * C, s));
+    A = ws;
+  }
+  GemmPair p{};
+  p.nprob = 1;
+  p.p[0] = problem(A, contiguous_rows(C), w->in_w, w->in_b, x_img, contiguous_rows(D), M, D, C);
+  HIP_TRY(gemm(p, EPI_STORE, c->dtype, false, s));
+  return DIT_OK;
+}
+
+dit_status run_final(const dit_block_config* c, const dit_step_weights* w, int B, int C, const float* temb,
+                     const void* x_img, float* v, char* ws, hipStream_t s) {
+  const int D = c->hidden;
+  float* s1 = (float*)ws;
+  float* fm = (float*)(ws + al256((size_t)B * D * 4));
+  char* h = ws + al256((size_t)B * D * 4) + al256((size_t)B * 2 * D * 4);
+  HIP_TRY(silu_f32(temb, s1, (int64_t)B * D, s));
+  GemvArgs g{};
+  g.W[0] = w->fmod_w;
+  g.bias[0] = w->fmod_b;
+  g.out[0] = fm;
+  g.out_bstride = 2 * D;
+  g.in = s1;
+  g.in_bstride = D;
+  g.N = 2 * D;
+  g.K = D;
+  g.B = B;
+  g.nstreams = 1;
+  HIP_TRY(gemv(g, c->dtype, s));
+  LnArgs a{};
+  a.x[0] = x_img;
+  a.xmap[0] = stream_rows(c->n_img, D);
+  a.out = h;
+  a.omap[0] = stream_rows(c->n_img, D);
+  a.mod[0] = fm;
+  a.mod_bstride = 2 * D;
+  a.shift_off = 0;
+  a.scale_off = D;
+  a.rows[0] = (int64_t)B * c->n_img;
+  a.rows[1] = 0;
+  a.D = D;
+  a.eps = c->ln_eps;
+  HIP_TRY(ln_modulate(a, c->dtype, s));
+  GemmPair p{};
+  p.nprob = 1;
+  p.p[0] = problem(h, contiguous_rows(D), w->fout_w, w->fout_b, v, contiguous_rows(C), B * c->n_img, C, D);
+  HIP_TRY(gemm(p, EPI_STORE, c->dtype, true, s));
+  return DIT_OK;
+}
+
+dit_status flow_coefficients(float t, float t_next, float a, bool has_noise, float* cx, float* cv, float* ce) {
+  if (!std::isfinite(t) || !std::isfinite(t_next) || !std::isfinite(a) || a < 0.f)
+    return fail(DIT_ERR_DOMAIN, "t, t_next and noise_level must be finite, noise_level >= 0");
+  if (t_next > t) return fail(DIT_ERR_DOMAIN, "t_next %g > t %g (the sampler runs from noise t=1 to data t=0)", t_next, t);
+  double h = (double)t_next - (double)t;
+  if (a == 0.f) {
+    *cx = 1.f;
+    *cv = (float)h;
+    *ce = 0.f;
+    return DIT_OK;
+  }
+  if (!(t > 0.f && t < 1.f)) return fail(DIT_ERR_DOMAIN, "SDE step needs 0 < t < 1 (t = %g)", t);
+  if (t_next < 0.f) return fail(DIT_ERR_DOMAIN, "t_next %g < 0", t_next);
+  if (!has_noise) return fail(DIT_ERR_INVALID_ARG, "noise is NULL with noise_level > 0");
+  double td = t, sigma = (double)a * std::sqrt(td / (1.0 - td));
+  double k = sigma * sigma / (2.0 * td);
+  // x + h (v + k (x + (1-t) v)) + sigma sqrt(-h) eps  =  (1 + h k) x + h (1 + k (1-t)) v + sigma sqrt(-h) eps
+  *cx = (float)(1.0 + h * k);
+  *cv = (float)(h * (1.0 + k * (1.0 - td)));
+  *ce = (float)(sigma * std::sqrt(-h));
+  return DIT_OK;
+}
+
+}  // namespace
+
+// ===========================================================================
+// exported entry points
+// ===========================================================================
+extern "C" {
+
+int32_t dit_abi_version(void) { return DIT_ABI_VERSION; }
+
+const char* dit_status_string(dit_status s) {
+  switch (s) {
+    case DIT_OK: return "ok";
+    case DIT_ERR_INVALID_ARG: return "invalid argument";
+    case DIT_ERR_SHAPE: return "inconsistent shape";
+    case DIT_ERR_DOMAIN: return "argument outside the domain";
+    case DIT_ERR_NAN: return "NaN or infinite input";
+    case DIT_ERR_UNSUPPORTED: return "unsupported configuration";
+    case DIT_ERR_HIP: return "HIP runtime error";
+    case DIT_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
+  }
+  return "unknown status";
+}
+
+const char* dit_last_error_message(void) { return g_err.c_str(); }
+
+size_t dit_block_workspace_bytes(const dit_block_config* cfg, int32_t batch) {
+  if (check_config(cfg) != DIT_OK || batch < 0) return 0;
+  return block_layout(cfg, batch).total;
+}
+
+dit_status dit_block_forward(const dit_block_config* c, const dit_block_weights* w, int32_t batch, const float* temb,
+                             void* x_img, void* x_txt, void* workspace, size_t workspace_bytes, dit_stream stream) {
+  dit_status st = check_block_args(c, w, batch, temb, x_img, x_txt);
+  if (st || batch == 0) return st;
+  BlockWs L = block_layout(c, batch);
+  if ((st = check_ws(workspace, workspace_bytes, L.total))) return st;
+  hipStream_t s = hs(stream);
+  char* ws = (char*)workspace;
+  const int B = batch, D = c->hidden, d = c->head_dim, H = c->heads;
+  const int S = c->n_img + c->n_txt;
+  const int rows[2] = {B * c->n_img, B * c->n_txt};
+  void* x[2] = {x_img, x_txt};
+  const int64_t nstream[2] = {c->n_img, c->n_txt};
+  float* mod = (float*)(ws + L.mod);
+  float* rope = (float*)(ws + L.rope);
+
+  if ((st = run_modulation(c, w, B, temb, ws, L, s))) return st;
+  if (c->rope) HIP_TRY(rope_table(rope, std::max(c->grid_h, c->grid_w), d, c->rope_theta, s));
+  // pre-attention LN + modulate into h
+  if ((st = run_ln(c, B, x_img, x_txt, ws, L, 0, D, s))) return st;
+  // QKV projection straight into the joint [B][S][3][H][d] buffer (+ RoPE on image q, k)
+  GemmPair qkv{};
+  qkv.nprob = 2;
+  for (int i = 0; i < 2; i++) {
+    qkv.p[i] = problem(ws + L.h, joint_rows(c, i, D), w->qkv_w[i], w->qkv_b[i], ws + L.qkv, joint_rows(c, i, 3 * D),
+                       rows[i], 3 * D, D);
+    qkv.p[i].head_dim = d;
+    qkv.p[i].hidden = D;
+    qkv.p[i].grid_w = c->grid_w;
+  }
+  if (c->rope) qkv.p[0].rope_tab = rope;
+  HIP_TRY(gemm(qkv, EPI_QKV, c->dtype, false, s));
+  // joint attention over [text ; image]; output o reuses the h buffer
+  AttnArgs at{};
+  char* qkvp = ws + L.qkv;
+  size_t es = esize(c->dtype);
+  at.q = qkvp;
+  at.k = qkvp + (size_t)D * es;
+  at.v = qkvp + (size_t)2 * D * es;
+  at.o = ws + L.h;
+  at.B = B;
+  at.H = H;
+  at.S = S;
+  at.d = d;
+  at.qs_b = (int64_t)S * 3 * D;
+  at.qs_s = 3 * D;
+  at.qs_h = d;
+  at.os_b = (int64_t)S * D;
+  at.os_s = D;
+  at.os_h = d;
+  at.scale = 1.0f / std::sqrt((float)d);
+  HIP_TRY(attention(at, c->dtype, s));
+  // output projection + gate1 residual, in place on x
+  GemmPair proj{};
+  proj.nprob = 2;
+  for (int i = 0; i < 2; i++) {
+    proj.p[i] = problem(ws + L.h, joint_rows(c, i, D), w->out_w[i], w->out_b[i], x[i], stream_rows(nstream[i], D),
+                        rows[i], D, D);
+    proj.p[i].gate = mod + (size_t)i * B * 6 * D + 2 * D;
+    proj.p[i].gate_bstride = 6 * D;
+  }
+  HIP_TRY(gemm(proj, EPI_RESID, c->dtype, false, s));
+  return run_mlp_half(c, w, B, x_img, x_txt, ws, L, s);
+}
+
+dit_status dit_block_mlp(const dit_block_config* c, const dit_block_weights* w, int32_t batch, const float* temb,
+                         void* x_img, void* x_txt, void* workspace, size_t workspace_bytes, dit_stream stream) {
+  dit_status st = check_block_args(c, w, batch, temb, x_img, x_txt);
+  if (st || batch == 0) return st;
+  BlockWs L = block_layout(c, batch);
+  if ((st = check_ws(workspace, workspace_bytes, L.total))) return st;
+  char* ws = (char*)workspace;
+  if ((st = run_modulation(c, w, batch, temb, ws, L, hs(stream)))) return st;
+  return run_mlp_half(c, w, batch, x_img, x_txt, ws, L, hs(stream));
+}
+
+dit_status joint_attention(const void* q, const void* k, const void* v, void* o, int32_t batch, int32_t heads,
+                           int32_t seq, int32_t head_dim, int64_t qkv_stride_b, int64_t qkv_stride_s,
+                           int64_t qkv_stride_h, int64_t o_stride_b, int64_t o_stride_s, int64_t o_stride_h,
+                           float scale, int32_t dtype, dit_stream stream) {
+  if (dtype != DIT_F32 && dtype != DIT_BF16) return fail(DIT_ERR_INVALID_ARG, "dtype %d invalid", dtype);
+  if (batch < 0 || heads < 0 || seq < 0) return fail(DIT_ERR_INVALID_ARG, "negative size");
+  if (head_dim != 64 && head_dim != 128) return fail(DIT_ERR_UNSUPPORTED, "head_dim %d (64 or 128)", head_dim);
+  if ((int64_t)batch * heads * seq == 0) return DIT_OK;
+  if (!q || !k || !v || !o) return fail(DIT_ERR_INVALID_ARG, "q/k/v/o NULL");
+  if (!std::isfinite(scale)) return fail(DIT_ERR_INVALID_ARG, "scale not finite");
+  size_t es = esize(dtype);
+  const int64_t strides[6] = {qkv_stride_b, qkv_stride_s, qkv_stride_h, o_stride_b, o_stride_s, o_stride_h};
+  for (int64_t st : strides)
+    if (st < 0 || (st * (int64_t)es) % 16) return fail(DIT_ERR_INVALID_ARG, "strides must be >= 0 and keep 16-byte rows");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o))
+    return fail(DIT_ERR_INVALID_ARG, "q/k/v/o must be 16-byte aligned");
+  AttnArgs a{};
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.o = o;
+  a.B = batch;
+  a.H = heads;
+  a.S = seq;
+  a.d = head_dim;
+  a.qs_b = qkv_stride_b;
+  a.qs_s = qkv_stride_s;
+  a.qs_h = qkv_stride_h;
+  a.os_b = o_stride_b;
+  a.os_s = o_stride_s;
+  a.os_h = o_stride_h;
+  a.scale = scale;
+  HIP_TRY(attention(a, dtype, hs(stream)));
+  return DIT_OK;
+}
+
+dit_status flow_step(float* x, const float* v, const float* noise, int64_t n, float t, float t_next,
+                     float noise_level, dit_stream stream) {
+  if (n < 0) return fail(DIT_ERR_INVALID_ARG, "n %lld < 0", (long long)n);
+  float cx, cv, ce;
+  dit_status st = flow_coefficients(t, t_next, noise_level, noise != nullptr, &cx, &cv, &ce);
+  if (st) return st;
+  if (n == 0) return DIT_OK;
+  if (!x || !v) return fail(DIT_ERR_INVALID_ARG, "x/v NULL");
+  HIP_TRY(flow_update(x, v, noise_level > 0.f ? noise : nullptr, n, cx, cv, ce, hs(stream)));
+  return DIT_OK;
+}
+
+dit_status group_reward_stats(const float* rewards, int32_t groups, int32_t n, float adv_eps, int32_t k_select,
+                              float* mean, float* stdv, float* adv, int32_t* order, int32_t* selected,
+                              dit_stream stream) {
+  if (groups < 0) return fail(DIT_ERR_INVALID_ARG, "groups %d < 0", groups);
+  if (n < 1 || n > 4096) return fail(DIT_ERR_INVALID_ARG, "n %d outside [1, 4096]", n);
+  if (k_select < 0 || k_select > n) return fail(DIT_ERR_INVALID_ARG, "k_select %d outside [0, n=%d]", k_select, n);
+  if (!(adv_eps >= 0.f) || !std::isfinite(adv_eps)) return fail(DIT_ERR_INVALID_ARG, "adv_eps must be >= 0");
+  if (groups == 0) return DIT_OK;
+  if (!rewards) return fail(DIT_ERR_INVALID_ARG, "rewards NULL");
+  hipStream_t s = hs(stream);
+  // NaN / Inf check on a host copy of the (small) input, before anything is written
+  std::vector<float> host((size_t)groups * n);
+  HIP_TRY(hipMemcpyAsync(host.data(), rewards, host.size() * 4, hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  for (size_t i = 0; i < host.size(); i++)
+    if (!std::isfinite(host[i])) return fail(DIT_ERR_NAN, "reward %zu (group %zu) is not finite", i % n, i / n);
+  HIP_TRY(reward_stats(rewards, groups, n, adv_eps, k_select, mean, stdv, adv, order, selected, s));
+  return DIT_OK;
+}
+
+dit_status dit_timestep_embed(const dit_block_config* c, const dit_step_weights* w, int32_t batch, const float* t,
+                              float* temb, void* workspace, size_t workspace_bytes, dit_stream stream) {
+  dit_status st = check_config(c);
+  if (st || (st = check_step_weights(w))) return st;
+  if (batch < 0) return fail(DIT_ERR_INVALID_ARG, "batch < 0");
+  if (batch == 0) return DIT_OK;
+  if (!t || !temb) return fail(DIT_ERR_INVALID_ARG, "t/temb NULL");
+  if ((st = check_ws(workspace, workspace_bytes, timestep_ws(c, batch)))) return st;
+  return run_timestep(c, w, batch, t, 0.f, temb, (char*)workspace, hs(stream));
+}
+
+dit_status dit_patch_embed(const dit_block_config* c, const dit_step_weights* w, int32_t batch, int32_t latent_dim,
+                           const float* latent, void* x_img, void* workspace, size_t workspace_bytes,
+                           dit_stream stream) {
+  dit_status st = check_config(c);
+  if (st || (st = check_step_weights(w))) return st;
+  if (batch < 0) return fail(DIT_ERR_INVALID_ARG, "batch < 0");
+  if (latent_dim <= 0 || latent_dim % 64) return fail(DIT_ERR_UNSUPPORTED, "latent_dim %d (multiple of 64)", latent_dim);
+  if (batch == 0) return DIT_OK;
+  if (!latent || !x_img || !aligned16(latent) || !aligned16(x_img))
+    return fail(DIT_ERR_INVALID_ARG, "latent/x_img NULL or not 16-byte aligned");
+  if ((st = check_ws(workspace, workspace_bytes, patch_ws(c, batch, latent_dim)))) return st;
+  return run_patch(c, w, batch, latent_dim, latent, x_img, (char*)workspace, hs(stream));
+}
+
+dit_status dit_final_layer(const dit_block_config* c, const dit_step_weights* w, int32_t batch, int32_t latent_dim,
+                           const float* temb, const void* x_img, float* v, void* workspace, size_t workspace_bytes,
+                           dit_stream stream) {
+  dit_status st = check_config(c);
+  if (st || (st = check_step_weights(w))) return st;
+  if (batch < 0) return fail(DIT_ERR_INVALID_ARG, "batch < 0");
+  if (latent_dim <= 0 || latent_dim % 64) return fail(DIT_ERR_UNSUPPORTED, "latent_dim %d (multiple of 64)", latent_dim);
+  if (batch == 0) return DIT_OK;
+  if (!temb || !x_img || !v || !aligned16(temb) || !aligned16(x_img) || !aligned16(v))
+    return fail(DIT_ERR_INVALID_ARG, "temb/x_img/v NULL or not 16-byte aligned");
+  if ((st = check_ws(workspace, workspace_bytes, final_ws(c, batch)))) return st;
+  return run_final(c, w, batch, latent_dim, temb, x_img, v, (char*)workspace, hs(stream));
+}
+
+size_t dit_denoise_workspace_bytes(const dit_block_config* c, int32_t batch, int32_t latent_dim) {
+  if (check_config(c) != DIT_OK || batch < 0 || latent_dim <= 0) return 0;
+  return step_layout(c, batch, latent_dim).total;
+}
+
+dit_status dit_denoise_step(const dit_block_config* c, const dit_step_weights* sw, const dit_block_weights* blocks,
+                            int32_t n_blocks, int32_t batch, int32_t latent_dim, float t, float t_next,
+                            float noise_level, float* latent, const void* x_txt, const float* noise, float* v_out,
+                            void* workspace, size_t workspace_bytes, dit_stream stream) {
+  dit_status st = check_config(c);
+  if (st || (st = check_step_weights(sw))) return st;
+  if (n_blocks < 0 || (n_blocks > 0 && !blocks)) return fail(DIT_ERR_INVALID_ARG, "blocks NULL or n_blocks < 0");
+  if (batch < 0) return fail(DIT_ERR_INVALID_ARG, "batch < 0");
+  if (latent_dim <= 0 || latent_dim % 64) return fail(DIT_ERR_UNSUPPORTED, "latent_dim %d (multiple of 64)", latent_dim);
+  float cx, cv, ce;
+  if ((st = flow_coefficients(t, t_next, noise_level, noise != nullptr, &cx, &cv, &ce))) return st;
+  if (batch == 0) return DIT_OK;
+  if (!latent || !aligned16(latent) || (c->n_txt > 0 && (!x_txt || !aligned16(x_txt))) ||
+      (v_out && !aligned16(v_out)))
+    return fail(DIT_ERR_INVALID_ARG, "latent/x_txt/v_out NULL or not 16-byte aligned");
+  StepWs L = step_layout(c, batch, latent_dim);
+  if ((st = check_ws(workspace, workspace_bytes, L.total))) return st;
+  char* ws = (char*)workspace;
+  float* temb = (float*)(ws + L.temb);
+  void* ximg = ws + L.ximg;
+  void* xtxt = ws + L.xtxt;
+  float* v = v_out ? v_out : (float*)(ws + L.v);
+  char* inner = ws + L.inner;
+  for (int i = 0; i < n_blocks; i++)
+    if ((st = check_block_args(c, &blocks[i], batch, temb, ximg, xtxt))) return st;
+  hipStream_t s = hs(stream);
+  const int B = batch, C = latent_dim;
+  if ((st = run_timestep(c, sw, B, nullptr, t, temb, inner, s))) return st;
+  if ((st = run_patch(c, sw, B, C, latent, ximg, inner, s))) return st;
+  if (c->n_txt > 0)
+    HIP_TRY(hipMemcpyAsync(xtxt, x_txt, (size_t)B * c->n_txt * c->hidden * esize(c->dtype), hipMemcpyDeviceToDevice, s));
+  size_t inner_bytes = workspace_bytes - L.inner;
+  for (int i = 0; i < n_blocks; i++)
+    if ((st = dit_block_forward(c, &blocks[i], B, temb, ximg, xtxt, inner, inner_bytes, stream))) return st;
+  if ((st = run_final(c, sw, B, C, temb, ximg, v, inner, s))) return st;
+  HIP_TRY(flow_update(latent, v, noise_level > 0.f ? noise : nullptr, (int64_t)B * c->n_img * C, cx, cv, ce, s));
+  return DIT_OK;
+}
+
+}  // extern "C"

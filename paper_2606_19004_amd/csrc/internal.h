@@ -1,0 +1,119 @@
+// Internal interfaces between the C ABI layer (api.hip) and the gfx950 kernels.
+// Nothing here crosses the library boundary.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace dit {
+
+typedef unsigned short u16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// ---------------------------------------------------------------------------
+// element access: bf16 storage (as u16 bits) or fp32, math always in fp32
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float to_f32(float x) { return x; }
+__device__ __forceinline__ float to_f32(u16 x) { return __uint_as_float(((uint32_t)x) << 16); }
+template <typename T> __device__ __forceinline__ T from_f32(float x);
+template <> __device__ __forceinline__ float from_f32<float>(float x) { return x; }
+template <> __device__ __forceinline__ u16 from_f32<u16>(float x) {
+  return __builtin_bit_cast(u16, (__bf16)x);  // round to nearest even (v_cvt_pk_bf16_f32)
+}
+
+// ---------------------------------------------------------------------------
+// row addressing: logical row m of a [rows][cols] operand lives at element
+//   (m / rows_per_batch) * batch_stride + (m % rows_per_batch) * row_stride + offset
+// which lets one stream's tokens be a strided slice of a joint [B][S][...] buffer.
+// ---------------------------------------------------------------------------
+struct RowMap {
+  int64_t rows_per_batch;
+  int64_t batch_stride;
+  int64_t row_stride;
+  int64_t offset;
+};
+__host__ __device__ __forceinline__ int64_t row_offset(const RowMap& r, int64_t m) {
+  int64_t b = m / r.rows_per_batch;
+  return b * r.batch_stride + (m - b * r.rows_per_batch) * r.row_stride + r.offset;
+}
+inline RowMap contiguous_rows(int64_t cols) { return RowMap{1, cols, 0, 0}; }
+
+__host__ __device__ __forceinline__ int cdiv(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
+
+// ---------------------------------------------------------------------------
+// GEMM: C[m][n] = epilogue( sum_k A[m][k] W[n][k] + bias[n] ), W stored [N][K]
+// ---------------------------------------------------------------------------
+enum Epi { EPI_STORE = 0, EPI_GELU = 1, EPI_RESID = 2, EPI_QKV = 3 };
+
+struct GemmProblem {
+  const void* A;  RowMap amap;   // rows of A (K contiguous)
+  const void* W;                 // [N][K] contiguous
+  const void* bias;              // [N] (weight dtype) or null
+  void* C;        RowMap cmap;   // output rows (N contiguous)
+  int M, N, K;
+  // EPI_RESID: C = C + gate[b][n] * y with b = m / cmap.rows_per_batch
+  const float* gate; int64_t gate_bstride;
+  // EPI_QKV: 2D RoPE on columns [0, 2*hidden) (q and k) of image rows
+  const float* rope_tab;         // [npos][head_dim/4] pairs (cos, sin), null = no RoPE
+  int grid_w, head_dim, hidden;
+};
+
+struct GemmPair {              // up to two problems (image stream, text stream) in one launch
+  GemmProblem p[2];
+  int nprob;
+};
+
+enum Dtype { DT_F32 = 0, DT_BF16 = 1 };
+
+hipError_t gemm(const GemmPair& pr, int epi, int dtype, bool out_f32, hipStream_t s);
+
+// ---------------------------------------------------------------------------
+// attention
+// ---------------------------------------------------------------------------
+struct AttnArgs {
+  const void* q; const void* k; const void* v; void* o;
+  int B, H, S, d;
+  int64_t qs_b, qs_s, qs_h;
+  int64_t os_b, os_s, os_h;
+  float scale;
+};
+hipError_t attention(const AttnArgs& a, int dtype, hipStream_t s);
+
+// ---------------------------------------------------------------------------
+// memory-bound kernels
+// ---------------------------------------------------------------------------
+// LayerNorm (no affine) + modulate over the rows of up to two streams.
+// out = LN(x)(1 + scale[b]) + shift[b]; shift at mod[s] + b*mod_bstride + shift_off.
+struct LnArgs {
+  const void* x[2]; RowMap xmap[2];
+  void* out;        RowMap omap[2];
+  const float* mod[2]; int64_t mod_bstride; int shift_off, scale_off;
+  int64_t rows[2];     // rows per stream (B * N_s)
+  int D; float eps;
+};
+hipError_t ln_modulate(const LnArgs& a, int dtype, hipStream_t s);
+
+// out[s][b][n] = sum_k W[s][n][k] in[b][k] + bias[s][n]  (fp32 in/out, W in weight dtype)
+struct GemvArgs {
+  const void* W[2]; const void* bias[2]; float* out[2];
+  int64_t out_bstride;
+  const float* in; int64_t in_bstride;
+  int N, K, B, nstreams;
+};
+hipError_t gemv(const GemvArgs& a, int dtype, hipStream_t s);
+
+hipError_t silu_f32(const float* in, float* out, int64_t n, hipStream_t s);
+hipError_t cast_f32_to_bf16(const float* in, u16* out, int64_t n, hipStream_t s);
+hipError_t timestep_sinusoid(const float* t_dev, float t_scalar, float* e, int B, hipStream_t s);
+hipError_t rope_table(float* tab, int npos, int head_dim, float theta, hipStream_t s);
+hipError_t flow_update(float* x, const float* v, const float* noise, int64_t n,
+                       float cx, float cv, float ce, hipStream_t s);
+hipError_t reward_stats(const float* r, int G, int n, float adv_eps, int k,
+                        float* mean, float* stdv, float* adv, int32_t* order, int32_t* sel,
+                        hipStream_t s);
+
+}  // namespace dit

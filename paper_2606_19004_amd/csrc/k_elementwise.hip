@@ -1,0 +1,385 @@
+// Memory-bound and latency-bound kernels of the denoise step for gfx950:
+//   flow_update    fused Euler / SDE latent update (fp32, 16-byte vector access)
+//   ln_modulate    LayerNorm (fp32 statistics) + adaLN modulate, one wave per row
+//   gemv           batched GEMV for the adaLN / timestep / final modulation vectors
+//   reward_stats   per prompt-group mean, std, advantages, stable descending ranks
+//   small helpers  SiLU, fp32->bf16 cast, timestep sinusoid, RoPE cos/sin table
+#include "internal.h"
+
+namespace dit {
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// ---------------------------------------------------------------------------
+// flow update: x' = cx*x + cv*v + ce*noise. The host folds the sampler step
+// (Euler ODE or reverse-time SDE, both linear in x, v and noise) into these
+// three coefficients in double precision.
+// ---------------------------------------------------------------------------
+template <bool NOISE>
+__global__ void __launch_bounds__(256) flow_update_vec(float4* __restrict__ x, const float4* __restrict__ v,
+                                                       const float4* __restrict__ e, int64_t n4,
+                                                       float cx, float cv, float ce) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += (int64_t)gridDim.x * 256) {
+    float4 a = x[i], b = v[i];
+    float4 r;
+    r.x = fmaf(cx, a.x, cv * b.x);
+    r.y = fmaf(cx, a.y, cv * b.y);
+    r.z = fmaf(cx, a.z, cv * b.z);
+    r.w = fmaf(cx, a.w, cv * b.w);
+    if (NOISE) {
+      float4 c = e[i];
+      r.x = fmaf(ce, c.x, r.x);
+      r.y = fmaf(ce, c.y, r.y);
+      r.z = fmaf(ce, c.z, r.z);
+      r.w = fmaf(ce, c.w, r.w);
+    }
+    x[i] = r;
+  }
+}
+
+__global__ void flow_update_tail(float* x, const float* v, const float* e, int64_t start, int64_t n,
+                                 float cx, float cv, float ce) {
+  int64_t i = start + threadIdx.x;
+  if (i < n) {
+    float r = fmaf(cx, x[i], cv * v[i]);
+    if (e) r = fmaf(ce, e[i], r);
+    x[i] = r;
+  }
+}
+
+__global__ void flow_update_scalar(float* x, const float* v, const float* e, int64_t n,
+                                   float cx, float cv, float ce) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) {
+    float r = fmaf(cx, x[i], cv * v[i]);
+    if (e) r = fmaf(ce, e[i], r);
+    x[i] = r;
+  }
+}
+
+hipError_t flow_update(float* x, const float* v, const float* noise, int64_t n, float cx, float cv, float ce,
+                       hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  bool aligned = ((uintptr_t)x % 16 == 0) && ((uintptr_t)v % 16 == 0) && (!noise || (uintptr_t)noise % 16 == 0);
+  if (aligned) {
+    int64_t n4 = n / 4;
+    if (n4 > 0) {
+      int grid = (int)std::min<int64_t>(cdiv(n4, 256), 4096);
+      if (noise)
+        flow_update_vec<true><<<grid, 256, 0, s>>>((float4*)x, (const float4*)v, (const float4*)noise, n4, cx, cv, ce);
+      else
+        flow_update_vec<false><<<grid, 256, 0, s>>>((float4*)x, (const float4*)v, nullptr, n4, cx, cv, ce);
+    }
+    if (n % 4) flow_update_tail<<<1, 64, 0, s>>>(x, v, noise, n4 * 4, n, cx, cv, ce);
+  } else {
+    int grid = (int)std::min<int64_t>(cdiv(n, 256), 4096);
+    flow_update_scalar<<<grid, 256, 0, s>>>(x, v, noise, n, cx, cv, ce);
+  }
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// small helpers
+// ---------------------------------------------------------------------------
+__global__ void silu_kernel(const float* __restrict__ in, float* __restrict__ out, int64_t n) {
+  int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) {
+    float z = in[i];
+    out[i] = z / (1.0f + __expf(-z));
+  }
+}
+hipError_t silu_f32(const float* in, float* out, int64_t n, hipStream_t s) {
+  if (n > 0) silu_kernel<<<cdiv(n, 256), 256, 0, s>>>(in, out, n);
+  return hipGetLastError();
+}
+
+__global__ void cast_bf16_kernel(const float* __restrict__ in, u16* __restrict__ out, int64_t n) {
+  int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) out[i] = from_f32<u16>(in[i]);
+}
+hipError_t cast_f32_to_bf16(const float* in, u16* out, int64_t n, hipStream_t s) {
+  if (n > 0) cast_bf16_kernel<<<cdiv(n, 256), 256, 0, s>>>(in, out, n);
+  return hipGetLastError();
+}
+
+// e[b] = [cos(1000 t f_j) ; sin(1000 t f_j)], f_j = 10000^(-j/128), evaluated in fp64.
+__global__ void sinusoid_kernel(const float* t_dev, float t_scalar, float* e, int B) {
+  int b = blockIdx.x, j = threadIdx.x;  // 128 threads
+  double t = t_dev ? (double)t_dev[b] : (double)t_scalar;
+  double f = exp(-log(10000.0) * (double)j / 128.0);
+  double arg = 1000.0 * t * f;
+  e[(int64_t)b * 256 + j] = (float)cos(arg);
+  e[(int64_t)b * 256 + 128 + j] = (float)sin(arg);
+}
+hipError_t timestep_sinusoid(const float* t_dev, float t_scalar, float* e, int B, hipStream_t s) {
+  if (B > 0) sinusoid_kernel<<<B, 128, 0, s>>>(t_dev, t_scalar, e, B);
+  return hipGetLastError();
+}
+
+// tab[pos][i] = (cos, sin)(pos * theta^(-2i/m)), m = head_dim/2, i < m/2, in fp64.
+__global__ void rope_table_kernel(float* tab, int npos, int head_dim, float theta) {
+  int pairs = head_dim / 4;
+  int idx = blockIdx.x * 256 + threadIdx.x;
+  if (idx >= npos * pairs) return;
+  int pos = idx / pairs, i = idx % pairs;
+  double m = head_dim / 2;
+  double ang = (double)pos * pow((double)theta, -2.0 * i / m);
+  tab[2 * idx] = (float)cos(ang);
+  tab[2 * idx + 1] = (float)sin(ang);
+}
+hipError_t rope_table(float* tab, int npos, int head_dim, float theta, hipStream_t s) {
+  int n = npos * (head_dim / 4);
+  if (n > 0) rope_table_kernel<<<cdiv(n, 256), 256, 0, s>>>(tab, npos, head_dim, theta);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// LayerNorm + modulate. One 64-lane wave per row; each lane owns CH chunks of
+// 8 consecutive elements (16-byte bf16 or 32-byte fp32 accesses), so a row of
+// D <= 512*CH stays in registers for the two-pass mean / variance.
+// ---------------------------------------------------------------------------
+template <typename T> struct Vec8;
+template <> struct Vec8<u16> {
+  static __device__ __forceinline__ void load(const u16* p, float* f) {
+    uint4 u = *(const uint4*)p;
+    uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+      f[2 * i] = __uint_as_float(w[i] << 16);
+      f[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+    }
+  }
+  static __device__ __forceinline__ void store(u16* p, const float* f) {
+    uint32_t w[4];
+#pragma unroll
+    for (int i = 0; i < 4; i++)
+      w[i] = (uint32_t)from_f32<u16>(f[2 * i]) | ((uint32_t)from_f32<u16>(f[2 * i + 1]) << 16);
+    *(uint4*)p = make_uint4(w[0], w[1], w[2], w[3]);
+  }
+};
+template <> struct Vec8<float> {
+  static __device__ __forceinline__ void load(const float* p, float* f) {
+    float4 a = *(const float4*)p, b = *(const float4*)(p + 4);
+    f[0] = a.x; f[1] = a.y; f[2] = a.z; f[3] = a.w; f[4] = b.x; f[5] = b.y; f[6] = b.z; f[7] = b.w;
+  }
+  static __device__ __forceinline__ void store(float* p, const float* f) {
+    *(float4*)p = make_float4(f[0], f[1], f[2], f[3]);
+    *(float4*)(p + 4) = make_float4(f[4], f[5], f[6], f[7]);
+  }
+};
+
+template <typename T, int CH>
+__global__ void __launch_bounds__(256) ln_modulate_kernel(LnArgs a) {
+  int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  int lane = threadIdx.x & 63;
+  int64_t total = a.rows[0] + a.rows[1];
+  if (row >= total) return;
+  int s = row < a.rows[0] ? 0 : 1;
+  int64_t m = s == 0 ? row : row - a.rows[0];
+  int64_t b = m / a.xmap[s].rows_per_batch;
+  const T* x = (const T*)a.x[s] + row_offset(a.xmap[s], m);
+  T* out = (T*)a.out + row_offset(a.omap[s], m);
+  const float* shift = a.mod[s] + b * a.mod_bstride + a.shift_off;
+  const float* scale = a.mod[s] + b * a.mod_bstride + a.scale_off;
+  const int D = a.D;
+
+  float v[CH][8];
+  float sum = 0.f;
+#pragma unroll
+  for (int c = 0; c < CH; c++) {
+    int k = (c * 64 + lane) * 8;
+    if (k < D) {
+      Vec8<T>::load(x + k, v[c]);
+#pragma unroll
+      for (int i = 0; i < 8; i++) sum += v[c][i];
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; i++) v[c][i] = 0.f;
+    }
+  }
+  float mean = wave_sum(sum) / (float)D;
+  float sq = 0.f;
+#pragma unroll
+  for (int c = 0; c < CH; c++) {
+    int k = (c * 64 + lane) * 8;
+    if (k < D) {
+#pragma unroll
+      for (int i = 0; i < 8; i++) {
+        float d = v[c][i] - mean;
+        sq += d * d;
+      }
+    }
+  }
+  float rstd = rsqrtf(wave_sum(sq) / (float)D + a.eps);
+#pragma unroll
+  for (int c = 0; c < CH; c++) {
+    int k = (c * 64 + lane) * 8;
+    if (k < D) {
+      float4 sh0 = *(const float4*)(shift + k), sh1 = *(const float4*)(shift + k + 4);
+      float4 sc0 = *(const float4*)(scale + k), sc1 = *(const float4*)(scale + k + 4);
+      float sh[8] = {sh0.x, sh0.y, sh0.z, sh0.w, sh1.x, sh1.y, sh1.z, sh1.w};
+      float sc[8] = {sc0.x, sc0.y, sc0.z, sc0.w, sc1.x, sc1.y, sc1.z, sc1.w};
+      float o[8];
+#pragma unroll
+      for (int i = 0; i < 8; i++) o[i] = fmaf((v[c][i] - mean) * rstd, 1.0f + sc[i], sh[i]);
+      Vec8<T>::store(out + k, o);
+    }
+  }
+}
+
+template <typename T>
+static hipError_t ln_launch(const LnArgs& a, hipStream_t s) {
+  int64_t total = a.rows[0] + a.rows[1];
+  if (total == 0) return hipSuccess;
+  int grid = cdiv(total, 4);
+  int ch = cdiv(a.D, 512);
+  if (ch <= 1) ln_modulate_kernel<T, 1><<<grid, 256, 0, s>>>(a);
+  else if (ch <= 2) ln_modulate_kernel<T, 2><<<grid, 256, 0, s>>>(a);
+  else if (ch <= 4) ln_modulate_kernel<T, 4><<<grid, 256, 0, s>>>(a);
+  else if (ch <= 6) ln_modulate_kernel<T, 6><<<grid, 256, 0, s>>>(a);
+  else ln_modulate_kernel<T, 8><<<grid, 256, 0, s>>>(a);
+  return hipGetLastError();
+}
+hipError_t ln_modulate(const LnArgs& a, int dtype, hipStream_t s) {
+  return dtype == DT_BF16 ? ln_launch<u16>(a, s) : ln_launch<float>(a, s);
+}
+
+// ---------------------------------------------------------------------------
+// batched GEMV: out[s][b][n] = W[s][n][:] . in[b][:] + bias[s][n], B <= 16 per
+// pass. A wave owns 4 weight rows and streams them once (16-byte loads), with
+// the fp32 input read through L1/L2; lanes split K and reduce at the end.
+// ---------------------------------------------------------------------------
+template <typename T, int BMAX>
+__global__ void __launch_bounds__(256) gemv_kernel(GemvArgs a, int b0, int nb) {
+  constexpr int R = 4;
+  int s = blockIdx.y;
+  int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  int n0 = (blockIdx.x * 4 + wave) * R;
+  if (n0 >= a.N) return;
+  const T* W = (const T*)a.W[s];
+  float acc[R][BMAX];
+#pragma unroll
+  for (int r = 0; r < R; r++)
+#pragma unroll
+    for (int b = 0; b < BMAX; b++) acc[r][b] = 0.f;
+  for (int k = lane * 8; k < a.K; k += 512) {
+    float w[R][8];
+#pragma unroll
+    for (int r = 0; r < R; r++) {
+      if (n0 + r < a.N) Vec8<T>::load(W + (int64_t)(n0 + r) * a.K + k, w[r]);
+      else
+#pragma unroll
+        for (int i = 0; i < 8; i++) w[r][i] = 0.f;
+    }
+#pragma unroll
+    for (int b = 0; b < BMAX; b++) {
+      if (b < nb) {
+        float x[8];
+        Vec8<float>::load(a.in + (int64_t)(b0 + b) * a.in_bstride + k, x);
+#pragma unroll
+        for (int r = 0; r < R; r++)
+#pragma unroll
+          for (int i = 0; i < 8; i++) acc[r][b] = fmaf(w[r][i], x[i], acc[r][b]);
+      }
+    }
+  }
+  const T* bias = (const T*)a.bias[s];
+#pragma unroll
+  for (int r = 0; r < R; r++) {
+#pragma unroll
+    for (int b = 0; b < BMAX; b++) {
+      float v = wave_sum(acc[r][b]);
+      if (lane == 0 && b < nb && n0 + r < a.N) {
+        if (bias) v += to_f32(bias[n0 + r]);
+        a.out[s][(int64_t)(b0 + b) * a.out_bstride + n0 + r] = v;
+      }
+    }
+  }
+}
+
+template <typename T>
+static hipError_t gemv_launch(const GemvArgs& a, hipStream_t s) {
+  dim3 grid(cdiv(a.N, 16), a.nstreams);
+  for (int b0 = 0; b0 < a.B; b0 += 16) {
+    int nb = std::min(16, a.B - b0);
+    if (nb <= 4) gemv_kernel<T, 4><<<grid, 256, 0, s>>>(a, b0, nb);
+    else if (nb <= 8) gemv_kernel<T, 8><<<grid, 256, 0, s>>>(a, b0, nb);
+    else gemv_kernel<T, 16><<<grid, 256, 0, s>>>(a, b0, nb);
+  }
+  return hipGetLastError();
+}
+hipError_t gemv(const GemvArgs& a, int dtype, hipStream_t s) {
+  if (a.N == 0 || a.B == 0) return hipSuccess;
+  return dtype == DT_BF16 ? gemv_launch<u16>(a, s) : gemv_launch<float>(a, s);
+}
+
+// ---------------------------------------------------------------------------
+// per-group reward statistics. One 256-thread workgroup per group; rewards of
+// the group in LDS; fp64 sums; rank of seed i = #{j : r_j > r_i or
+// (r_j == r_i and j < i)}, so order[rank_i] = i is the stable descending sort
+// (ties by index), computed without atomics and bit-exactly.
+// ---------------------------------------------------------------------------
+__device__ double block_sum_f64(double v, double* red) {
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  int w = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[w] = v;
+  __syncthreads();
+  return red[0] + red[1] + red[2] + red[3];
+}
+
+__global__ void __launch_bounds__(256) reward_stats_kernel(const float* __restrict__ rw, int n, float adv_eps,
+                                                           int k, float* mean, float* stdv, float* adv,
+                                                           int32_t* order, int32_t* sel) {
+  extern __shared__ float sr[];               // n rewards, then n ints of order
+  __shared__ double red[4];
+  int32_t* so = (int32_t*)(sr + n);
+  int g = blockIdx.x;
+  const float* r = rw + (int64_t)g * n;
+  double part = 0.0;
+  for (int i = threadIdx.x; i < n; i += 256) {
+    float x = r[i];
+    sr[i] = x;
+    part += (double)x;
+  }
+  double mu = block_sum_f64(part, red) / (double)n;   // block_sum syncs after the LDS fill
+  part = 0.0;
+  for (int i = threadIdx.x; i < n; i += 256) {
+    double d = (double)sr[i] - mu;
+    part += d * d;
+  }
+  double sd = sqrt(block_sum_f64(part, red) / (double)n);
+  if (threadIdx.x == 0) {
+    if (mean) mean[g] = (float)mu;
+    if (stdv) stdv[g] = (float)sd;
+  }
+  for (int i = threadIdx.x; i < n; i += 256) {
+    float ri = sr[i];
+    if (adv) adv[(int64_t)g * n + i] = sd > 0.0 ? (float)(((double)ri - mu) / (sd + (double)adv_eps)) : 0.0f;
+    int rank = 0;
+    for (int j = 0; j < n; j++) {
+      float rj = sr[j];
+      rank += (rj > ri) || (rj == ri && j < i);
+    }
+    so[rank] = i;
+  }
+  __syncthreads();
+  int top = (k + 1) / 2;
+  for (int i = threadIdx.x; i < n; i += 256)
+    if (order) order[(int64_t)g * n + i] = so[i];
+  for (int q = threadIdx.x; q < k; q += 256)
+    if (sel) sel[(int64_t)g * k + q] = so[q < top ? q : n - k + q];
+}
+
+hipError_t reward_stats(const float* r, int G, int n, float adv_eps, int k, float* mean, float* stdv,
+                        float* adv, int32_t* order, int32_t* sel, hipStream_t s) {
+  if (G == 0) return hipSuccess;
+  size_t lds = (size_t)n * 8;
+  reward_stats_kernel<<<G, 256, lds, s>>>(r, n, adv_eps, k, mean, stdv, adv, order, sel);
+  return hipGetLastError();
+}
+
+}  // namespace dit

@@ -1,0 +1,89 @@
+"""GPU parity: joint_attention against the oracle's softmax attention."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import seeded_inputs as si
+from oracle import dit_oracle as O
+from tests.gpu_util import dev, host64, rel_err
+
+pytestmark = pytest.mark.gpu
+
+# bf16 inputs, bf16 P before the PV product and a bf16 output: ~2^-8 relative per
+# rounding, averaged over many keys; 1e-2 leaves a wide margin, a layout bug gives O(1).
+TOL_BF16 = 1e-2
+TOL_F32 = 1e-5
+
+
+@pytest.fixture(scope="module")
+def d():
+    from paper_2606_19004_amd import ditstep
+    return ditstep
+
+
+def _packed(rng, b, s, h, hd, dtype):
+    """A packed [B][S][3][H][d] buffer like the block's QKV output."""
+    x = rng.standard_normal((b, s, 3, h, hd)).astype(np.float32)
+    return si.stored(x, dtype)
+
+
+def _run(d, qkv_store, b, s, h, hd, dtype):
+    buf = dev(qkv_store, dtype)
+    o = torch.zeros((b, s, h * hd), dtype=buf.dtype, device="cuda")
+    D = h * hd
+    flat = buf.view(-1)
+    d.joint_attention(flat[0:], flat[D:], flat[2 * D:], o, b, h, s, hd, (s * 3 * D, 3 * D, hd), (s * D, D, hd),
+                      dtype=dtype)
+    return host64(o).reshape(b, s, h, hd)
+
+
+@pytest.mark.parametrize("b,s,h,hd", [(2, 200, 3, 128), (1, 64, 2, 128), (3, 77, 5, 64), (1, 1, 1, 128),
+                                      (2, 385, 2, 64)])
+def test_attention_bf16_small(d, b, s, h, hd):
+    rng = np.random.default_rng(s * 7 + hd)
+    st = _packed(rng, b, s, h, hd, "bf16")
+    got = _run(d, st, b, s, h, hd, "bf16")
+    x = si.as_f64(st, "bf16")
+    for bi in range(b):
+        ref = O.joint_attention(x[bi, :, 0], x[bi, :, 1], x[bi, :, 2])
+        assert rel_err(got[bi], ref) <= TOL_BF16
+
+
+@pytest.mark.parametrize("b,s,h,hd", [(2, 80, 4, 64), (1, 45, 2, 128)])
+def test_attention_f32(d, b, s, h, hd):
+    rng = np.random.default_rng(s)
+    st = _packed(rng, b, s, h, hd, "f32")
+    got = _run(d, st, b, s, h, hd, "f32")
+    for bi in range(b):
+        ref = O.joint_attention(st[bi, :, 0].astype(np.float64), st[bi, :, 1].astype(np.float64),
+                                st[bi, :, 2].astype(np.float64))
+        assert rel_err(got[bi], ref) <= TOL_F32
+
+
+def test_attention_large_logits_stay_finite(d):
+    rng = np.random.default_rng(5)
+    x = rng.standard_normal((1, 300, 3, 2, 128)).astype(np.float32)
+    x[:, :, 0] *= 30.0       # scores of several hundred
+    st = si.stored(x, "bf16")
+    got = _run(d, st, 1, 300, 2, 128, "bf16")
+    xs = si.as_f64(st, "bf16")
+    ref = O.joint_attention(xs[0, :, 0], xs[0, :, 1], xs[0, :, 2])
+    assert np.all(np.isfinite(got))
+    assert rel_err(got[0], ref) <= TOL_BF16
+
+
+@pytest.mark.parametrize("name", ["block_1280", "headslice_1280"])
+def test_attention_full_size_sampled(d, name):
+    """Full 6912-token shapes; the oracle evaluates sampled query rows of a few (sample, head) pairs."""
+    cfg = si.CONFIGS[name]
+    b, s, h, hd = cfg.batch, cfg.seq, cfg.heads, cfg.head_dim
+    q = si.stored(si.normal(f"{name}/attn_qkv", (b, s, 3, h, hd)), "bf16")
+    got = _run(d, q, b, s, h, hd, "bf16")
+    rng = np.random.default_rng(11)
+    rows = np.r_[0, s - 1, rng.choice(s, 30, replace=False)]
+    for bi, hi in [(0, 0), (b - 1, h - 1), (b // 2, h // 2)]:
+        x = si.as_f64(q[bi, :, :, hi], "bf16")        # [S][3][d]
+        ref = O.attention(x[rows, 0], x[:, 1], x[:, 2])
+        assert rel_err(got[bi, rows, hi], ref) <= TOL_BF16

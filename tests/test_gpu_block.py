@@ -1,0 +1,184 @@
+"""GPU parity: dit_block_forward / dit_block_mlp against the oracle.
+
+Tolerances. The block contract is a normwise max relative error of 2e-2 on the
+block output (bf16 storage, fp32 accumulation). The branch delta (out - in)
+is gated too, at 2e-2 of max|delta| plus the unavoidable rounding of the bf16
+output itself (half an ulp, <= 2^-8 max|out|). The fp32 configuration is held
+to 1e-4."""
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+import seeded_inputs as si
+from oracle import dit_oracle as O
+from tests.conftest import weights_f64
+from tests.gpu_util import block_cfg, dev, host64, rel_err, upload_block
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def d():
+    from paper_2606_19004_amd import ditstep
+    return ditstep
+
+
+def tol(cfg):
+    return 2e-2 if cfg.dtype == "bf16" else 1e-4
+
+
+def check(cfg, got, ref, inp):
+    t = tol(cfg)
+    assert rel_err(got, ref) <= t, rel_err(got, ref)
+    floor = 2.0 ** -8 * np.max(np.abs(ref)) if cfg.dtype == "bf16" else 0.0
+    derr = np.max(np.abs((got - inp) - (ref - inp)))
+    assert derr <= t * np.max(np.abs(ref - inp)) + floor, (derr, np.max(np.abs(ref - inp)), floor)
+
+
+def run_block(d, cfg, inp, mlp_only=False):
+    c = block_cfg(d, cfg)
+    w = upload_block(inp["weights"], cfg.dtype)
+    bw = d.block_weights(w["img"], w["txt"])
+    temb = dev(inp["temb"])
+    xi, xt = dev(inp["x_img"], cfg.dtype), dev(inp["x_txt"], cfg.dtype)
+    ws = d.workspace(d.dit_block_workspace_bytes(c, cfg.batch))
+    (d.dit_block_mlp if mlp_only else d.dit_block_forward)(c, bw, temb, xi, xt, ws)
+    torch.cuda.synchronize()
+    return host64(xi), host64(xt), (c, bw, temb, xi, xt, ws, w)
+
+
+@pytest.mark.parametrize("name", ["tiny_f32", "small_bf16", "small_bf16_d64"])
+def test_block_small_full_compare(d, name):
+    cfg = si.CONFIGS[name]
+    inp = si.block_inputs(cfg)
+    gi, gt, _ = run_block(d, cfg, inp)
+    w64 = weights_f64(inp["weights"], cfg.dtype)
+    xi, xt = si.as_f64(inp["x_img"], cfg.dtype), si.as_f64(inp["x_txt"], cfg.dtype)
+    ri, rt = O.block_forward(cfg, w64, inp["temb"].astype(np.float64), xi, xt)
+    check(cfg, gi, ri, xi)
+    check(cfg, gt, rt, xt)
+
+
+@pytest.mark.parametrize("name", ["small_bf16", "tiny_f32"])
+def test_block_rope_off_and_no_text(d, name):
+    cfg = dataclasses.replace(si.CONFIGS[name], rope=False)
+    inp = si.block_inputs(cfg)
+    gi, gt, _ = run_block(d, cfg, inp)
+    w64 = weights_f64(inp["weights"], cfg.dtype)
+    xi, xt = si.as_f64(inp["x_img"], cfg.dtype), si.as_f64(inp["x_txt"], cfg.dtype)
+    ri, rt = O.block_forward(cfg, w64, inp["temb"].astype(np.float64), xi, xt)
+    check(cfg, gi, ri, xi)
+    # no text tokens at all: image-only self-attention
+    cfg0 = dataclasses.replace(si.CONFIGS[name], n_txt=0)
+    inp0 = si.block_inputs(cfg0)
+    gi0, _, _ = run_block(d, cfg0, inp0)
+    w0 = weights_f64(inp0["weights"], cfg0.dtype)
+    xi0 = si.as_f64(inp0["x_img"], cfg0.dtype)
+    ri0, _ = O.block_forward(cfg0, w0, inp0["temb"].astype(np.float64), xi0, np.zeros((cfg0.batch, 0, cfg0.hidden)))
+    check(cfg0, gi0, ri0, xi0)
+
+
+def test_block_adaln_zero_identity_bit_exact(d):
+    cfg = si.CONFIGS["small_bf16"]
+    inp = si.block_inputs(cfg)
+    D = cfg.hidden
+    for s in ("img", "txt"):
+        for chunk in (2, 5):    # gate1, gate2 rows and biases
+            inp["weights"][s]["mod_w"][chunk * D:(chunk + 1) * D] = 0
+            inp["weights"][s]["mod_b"][chunk * D:(chunk + 1) * D] = 0
+    gi, gt, _ = run_block(d, cfg, inp)
+    np.testing.assert_array_equal(gi, si.as_f64(inp["x_img"], "bf16"))
+    np.testing.assert_array_equal(gt, si.as_f64(inp["x_txt"], "bf16"))
+
+
+def test_block_deterministic(d):
+    cfg = si.CONFIGS["small_bf16"]
+    inp = si.block_inputs(cfg)
+    a = run_block(d, cfg, inp)
+    b = run_block(d, cfg, inp)
+    np.testing.assert_array_equal(a[0], b[0])
+    np.testing.assert_array_equal(a[1], b[1])
+
+
+def test_block_mlp_half(d):
+    cfg = si.CONFIGS["small_bf16"]
+    inp = si.block_inputs(cfg)
+    gi, gt, _ = run_block(d, cfg, inp, mlp_only=True)
+    w64 = weights_f64(inp["weights"], cfg.dtype)
+    temb = inp["temb"].astype(np.float64)
+    for s, g, x in (("img", gi, inp["x_img"]), ("txt", gt, inp["x_txt"])):
+        x64 = si.as_f64(x, cfg.dtype)
+        for b in range(cfg.batch):
+            m = {k: v[0] for k, v in O.modulation(temb[b:b + 1], w64[s]["mod_w"], w64[s]["mod_b"]).items()}
+            check(cfg, g[b], O.mlp_half(w64[s], m, x64[b]), x64[b])
+
+
+def test_block_errors_write_nothing(d):
+    cfg = si.CONFIGS["small_bf16"]
+    inp = si.block_inputs(cfg)
+    c = block_cfg(d, cfg)
+    w = upload_block(inp["weights"], cfg.dtype)
+    bw = d.block_weights(w["img"], w["txt"])
+    temb, xi, xt = dev(inp["temb"]), dev(inp["x_img"], "bf16"), dev(inp["x_txt"], "bf16")
+    before = xi.clone()
+    need = d.dit_block_workspace_bytes(c, cfg.batch)
+    with pytest.raises(d.DitError) as ei:
+        d.dit_block_forward(c, bw, temb, xi, xt, d.workspace(need - 256))
+    assert ei.value.name == "DIT_ERR_WORKSPACE"
+    bad = block_cfg(d, dataclasses.replace(cfg, grid_w=cfg.grid_w + 1))
+    with pytest.raises(d.DitError) as ei:
+        d.dit_block_forward(bad, bw, temb, xi, xt, d.workspace(need))
+    assert ei.value.name == "DIT_ERR_SHAPE"
+    torch.cuda.synchronize()
+    assert torch.equal(xi, before)
+
+
+def _sampled(cfg, inp, gi, gt, batches, n_rows=24):
+    w64 = weights_f64(inp["weights"], cfg.dtype)
+    rng = np.random.default_rng(7)
+    for b in batches:
+        ir = np.unique(np.r_[0, cfg.n_img - 1, rng.choice(cfg.n_img, n_rows, replace=False)])
+        tr = np.unique(np.r_[0, cfg.n_txt - 1, rng.choice(cfg.n_txt, n_rows // 3, replace=False)])
+        xi = si.as_f64(inp["x_img"][b], cfg.dtype)
+        xt = si.as_f64(inp["x_txt"][b], cfg.dtype)
+        ri, rt = O.block_forward_sample(cfg, w64, inp["temb"][b].astype(np.float64), xi, xt, ir, tr)
+        check(cfg, gi[b][ir], ri, xi[ir])
+        check(cfg, gt[b][tr], rt, xt[tr])
+
+
+@pytest.mark.parametrize("name", ["block_512", "block_1280"])
+def test_block_full_size_sampled(d, name):
+    cfg = si.CONFIGS[name]
+    inp = si.block_inputs(cfg)
+    gi, gt, _ = run_block(d, cfg, inp)
+    assert np.all(np.isfinite(gi)) and np.all(np.isfinite(gt))
+    _sampled(cfg, inp, gi, gt, [0, cfg.batch - 1])
+
+
+def test_block_step_shape_sampled(d):
+    """One block at the full-step launch shape (K=16, 1024 + 256 tokens)."""
+    cfg = dataclasses.replace(si.CONFIGS["step_512_k16"], blocks=1)
+    inp = si.block_inputs(cfg)
+    gi, gt, _ = run_block(d, cfg, inp)
+    _sampled(cfg, inp, gi, gt, [5])
+
+
+def test_mlp_slice_full_size_sampled(d):
+    """The per-token MLP half on one sequence-parallel rank's 1600 + 128 token slice."""
+    cfg = si.CONFIGS["mlp_slice_1280"]
+    inp = si.block_inputs(cfg)
+    gi, gt, _ = run_block(d, cfg, inp, mlp_only=True)
+    w64 = weights_f64(inp["weights"], cfg.dtype)
+    rng = np.random.default_rng(3)
+    for b in (0, cfg.batch - 1):
+        m = {}
+        for s in ("img", "txt"):
+            mm = O.modulation(inp["temb"][b:b + 1].astype(np.float64), w64[s]["mod_w"], w64[s]["mod_b"])
+            m[s] = {k: v[0] for k, v in mm.items()}
+        ir = rng.choice(cfg.n_img, 32, replace=False)
+        xi = si.as_f64(inp["x_img"][b], cfg.dtype)
+        check(cfg, gi[b][ir], O.mlp_half(w64["img"], m["img"], xi[ir]), xi[ir])
+        xt = si.as_f64(inp["x_txt"][b], cfg.dtype)
+        check(cfg, gt[b], O.mlp_half(w64["txt"], m["txt"], xt), xt)
