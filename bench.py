@@ -1,0 +1,206 @@
+#!/usr/bin/env python3
+"""Benchmark: milliseconds per K-seed DiT denoise step on one MI355X.
+
+One step = the whole hot path over one batch: timestep embedding, patch
+embedding, 8 dual-stream MMDiT blocks (hidden 3072, 24 heads x 128, 1024 image
++ 256 text tokens, K = 16 seeds), velocity head, SDE flow update (a = 0.7),
+then per-group reward statistics with argsort over 64 prompt groups x 16
+seeds. Inputs are synthetic and seeded (weights N(0, 0.02) in bf16, hidden
+states N(0, 1), rewards U(0, 1)), resident in HBM before timing starts.
+
+Prints ONE JSON line: the step time, the dominant kernel's roofline fraction
+(its algorithmic FLOPs per launch over its average launch time, timed with
+HIP events on its stream), a per-kernel-class breakdown, and the CPU oracle
+timed on a bounded sample of the same workload.
+
+    python bench.py [--steps K] [--warmup W] [--config NAME] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import seeded_inputs as si  # noqa: E402
+
+PEAK_BF16_TFLOPS = 2516.6      # MI355X dense bf16 MFMA (256 CUs x 2.4 GHz x 4096 flop/clk)
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--config", default="step_512_k16", choices=[k for k, v in si.CONFIGS.items() if v.blocks >= 1])
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-sample-seeds", type=int, default=1)
+    return p.parse_args()
+
+
+class DeviceInputs:
+    """Seeded synthetic inputs generated on the GPU with the recipe of seeded_inputs."""
+
+    def __init__(self, torch, d, cfg, seed=si.MASTER_SEED):
+        self.torch = torch
+        g = torch.Generator(device="cuda")
+        g.manual_seed(seed)
+        act = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+
+        def w(shape, std=0.02):
+            return (torch.randn(shape, generator=g, device="cuda", dtype=torch.float32) * std).to(act)
+
+        self.blocks_t = []
+        for _ in range(cfg.blocks):
+            self.blocks_t.append({s: {t: w(shp) for t, shp in si.block_weight_shapes(cfg).items()}
+                                  for s in si.STREAMS})
+        self.blocks = [d.block_weights(b["img"], b["txt"]) for b in self.blocks_t]
+        self.sw_t = {t: w(shp) for t, shp in si.step_weight_shapes(cfg).items()}
+        self.sw = d.step_weights(self.sw_t)
+        B = cfg.batch
+        self.latent = torch.randn((B, cfg.n_img, cfg.latent_dim), generator=g, device="cuda")
+        text = torch.randn((1, cfg.n_txt, cfg.hidden), generator=g, device="cuda").to(act)
+        self.x_txt = text.expand(B, -1, -1).contiguous()
+        self.eps = torch.randn((B, cfg.n_img, cfg.latent_dim), generator=g, device="cuda")
+        self.v = torch.empty_like(self.latent)
+        t = float(torch.rand((1,), generator=g, device="cuda").item())
+        self.t = min(max(t, 0.06), 0.94)
+        self.t_next = self.t - cfg.dt
+        G = max(cfg.reward_groups, 1)
+        n = max(cfg.reward_n, 1)
+        self.k = cfg.reward_k
+        self.rewards = torch.rand((G, n), generator=g, device="cuda")
+        self.mean = torch.empty(G, device="cuda")
+        self.std = torch.empty(G, device="cuda")
+        self.adv = torch.empty((G, n), device="cuda")
+        self.order = torch.empty((G, n), dtype=torch.int32, device="cuda")
+        self.selected = torch.empty((G, max(self.k, 1)), dtype=torch.int32, device="cuda")
+        self.cfg = d.block_config(cfg.hidden, cfg.heads, cfg.head_dim, cfg.mlp_hidden, cfg.n_img, cfg.n_txt,
+                                  cfg.grid_h, cfg.grid_w, rope=cfg.rope, dtype=cfg.dtype)
+        self.ws = d.workspace(d.dit_denoise_workspace_bytes(self.cfg, B, cfg.latent_dim))
+
+
+def make_step(d, cfg, x):
+    a = cfg.noise_level
+
+    def step():
+        d.dit_denoise_step(x.cfg, x.sw, x.blocks, x.t, x.t_next, a, x.latent, x.x_txt,
+                           x.eps if a > 0 else None, x.v, x.ws)
+        if cfg.reward_groups:
+            d.group_reward_stats(x.rewards, 1e-4, x.k, x.mean, x.std, x.adv, x.order, x.selected)
+    return step
+
+
+def cpu_baseline(cfg, n_seeds):
+    """Time the oracle on a bounded sample: one block for `n_seeds` seeds (all rows),
+    scaled to a full step (blocks x K seeds). Block work dominates the step."""
+    from oracle import dit_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    except Exception:  # noqa: BLE001
+        threads = os.cpu_count() or 1
+    import dataclasses
+    c1 = dataclasses.replace(cfg, blocks=1, batch=n_seeds)
+    inp = si.block_inputs(c1)
+    w64 = {s: {t: si.as_f64(a, c1.dtype) for t, a in ws.items()} for s, ws in inp["weights"].items()}
+    xi, xt = si.as_f64(inp["x_img"], c1.dtype), si.as_f64(inp["x_txt"], c1.dtype)
+    temb = inp["temb"].astype(np.float64)
+    t0 = time.perf_counter()
+    for b in range(n_seeds):
+        O.block_forward_sample(c1, w64, temb[b], xi[b], xt[b])
+    sec = time.perf_counter() - t0
+    per_seed_block = sec / n_seeds
+    ms_step = per_seed_block * cfg.blocks * cfg.batch * 1e3
+    return {"value": round(ms_step, 1), "unit": "ms per K-seed denoise step", "cores": int(threads), "kind": "oracle",
+            "sample": f"fp64 numpy oracle, one MMDiT block for {n_seeds} seed(s) at the step's shape "
+                      f"({cfg.seq} tokens, hidden {cfg.hidden}), {sec:.1f} s measured, scaled x{cfg.blocks} blocks "
+                      f"x{cfg.batch} seeds"}
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: this build runs the denoise step on a single MI355X "
+              "(no collectives); run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2606_19004_amd import ditstep as d
+    cfg = si.CONFIGS[args.config]
+    torch.cuda.set_device(0)
+    x = DeviceInputs(torch, d, cfg)
+    step = make_step(d, cfg, x)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms = elapsed * 1e3 / args.steps
+    print(f"timed {args.steps} steps: {ms:.3f} ms/step", file=sys.stderr, flush=True)
+
+    # per-kernel-class timing: one more step with HIP events around every launch
+    d.dit_profile_begin()
+    step()
+    stats = d.dit_profile_end()
+    kernels = {}
+    for k in stats:
+        avg = k["total_ms"] / k["launches"]
+        e = {"launches": k["launches"], "avg_us": round(avg * 1e3, 2), "total_ms": round(k["total_ms"], 4)}
+        if k["flops"] > 0:
+            e["tflops"] = round(k["flops"] / (k["total_ms"] * 1e-3) / 1e12, 1)
+            e["frac_mfma"] = round(e["tflops"] / PEAK_BF16_TFLOPS, 4)
+        if k["bytes"] > 0 and k["flops"] == 0:
+            e["gbs"] = round(k["bytes"] / (k["total_ms"] * 1e-3) / 1e9, 1)
+            e["frac_hbm"] = round(e["gbs"] / PEAK_HBM_GBS, 4)
+        kernels[k["name"]] = e
+    dom = max(stats, key=lambda k: k["total_ms"])
+    avg_s = dom["total_ms"] / dom["launches"] * 1e-3
+    per_launch = dom["flops"] / dom["launches"]
+    achieved = per_launch / avg_s / 1e12
+    roofline = {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None, "kernel": dom["name"],
+                "flops_per_launch": per_launch, "avg_launch_us": round(avg_s * 1e6, 2)}
+    gemm_ms = sum(k["total_ms"] for k in stats if k["name"].startswith("gemm"))
+    gemm_fl = sum(k["flops"] for k in stats if k["name"].startswith("gemm"))
+    attn = [k for k in stats if k["name"] == "attention"]
+    summary = {"gemm_tflops": round(gemm_fl / (gemm_ms * 1e-3) / 1e12, 1) if gemm_ms else None,
+               "attention_tflops": round(attn[0]["flops"] / (attn[0]["total_ms"] * 1e-3) / 1e12, 1) if attn else None}
+    summary["gemm_frac"] = round(summary["gemm_tflops"] / PEAK_BF16_TFLOPS, 4) if summary["gemm_tflops"] else None
+    summary["attention_frac"] = (round(summary["attention_tflops"] / PEAK_BF16_TFLOPS, 4)
+                                 if summary["attention_tflops"] else None)
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        print("timing the CPU oracle on a bounded sample ...", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(cfg, args.cpu_sample_seeds)
+
+    out = {
+        "metric": "ms per K-seed denoise step", "value": round(ms, 4), "unit": "ms", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": False,
+        "scaling": "weak", "vs_baseline": None, "dtype": cfg.dtype, "data": "synthetic",
+        "config": {"workload": (f"{cfg.name}: {cfg.blocks} dual-stream MMDiT blocks, hidden {cfg.hidden}, "
+                                f"{cfg.heads}x{cfg.head_dim} heads, {cfg.n_img} image + {cfg.n_txt} text tokens, "
+                                f"K={cfg.batch} seeds, flow update a={cfg.noise_level}, reward stats "
+                                f"{cfg.reward_groups}x{cfg.reward_n}"),
+                   "batch": cfg.batch, "seq_len": cfg.seq, "blocks": cfg.blocks, "parallelism": "single GPU"},
+        "roofline": roofline,
+        "mfma_summary": summary,
+        "kernels": kernels,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

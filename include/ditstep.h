@@ -228,6 +228,28 @@ dit_status dit_denoise_step(const dit_block_config* cfg, const dit_step_weights*
                             float noise_level, float* latent, const void* x_txt, const float* noise,
                             float* v_out, void* workspace, size_t workspace_bytes, dit_stream stream);
 
+/* ------------------------------------------------------------------ */
+/* kernel timing (benchmark instrumentation)                            */
+/* ------------------------------------------------------------------ */
+/* One kernel class (a family of launches: "gemm_mlp_up_gelu", "attention",
+ * ...) accumulated between dit_profile_begin and dit_profile_end. flops and
+ * bytes are ALGORITHMIC totals over those launches (2*M*N*K per GEMM,
+ * 4*B*H*S^2*d per attention, bytes each memory-bound kernel must move). */
+typedef struct {
+  char name[40];
+  int32_t launches;
+  double total_ms;   /* sum of per-launch durations, hipEvent pairs on the launch stream */
+  double flops;
+  double bytes;
+} dit_kernel_stat;
+
+/* Start recording: every library launch from now on is bracketed by a pair
+ * of hipEvents on its stream. Process-wide; not for concurrent callers. */
+dit_status dit_profile_begin(void);
+/* Stop recording, wait for the recorded events, and write up to `capacity`
+ * per-class totals (host array) plus their number to *count. */
+dit_status dit_profile_end(dit_kernel_stat* stats, int32_t capacity, int32_t* count);
+
 #ifdef __cplusplus
 }
 #endif

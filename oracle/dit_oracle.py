@@ -198,7 +198,7 @@ def block_forward_sample(cfg, w, temb_b, x_img_b, x_txt_b, img_rows=None, txt_ro
     out = {}
     for s in ("img", "txt"):
         r = rows[s]
-        o = joint_attention(q[s][r], k_joint, v_joint).reshape(len(r), -1)
+        o = joint_attention(q[s][r], k_joint, v_joint).reshape(len(r), heads * cfg.head_dim)
         xs = x[s][r] + mod[s]["gate1"] * linear(o, w[s]["out_w"], w[s]["out_b"])
         h2 = layer_norm(xs) * (1.0 + mod[s]["scale2"]) + mod[s]["shift2"]
         u = gelu_tanh(linear(h2, w[s]["mlp1_w"], w[s]["mlp1_b"]))

@@ -3,6 +3,9 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstring>
+#include <map>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -30,6 +33,41 @@ dit_status fail(dit_status s, const char* fmt, ...) {
     hipError_t e_ = (expr);                                                                   \
     if (e_ != hipSuccess) return fail(DIT_ERR_HIP, "%s failed: %s", #expr, hipGetErrorString(e_)); \
   } while (0)
+
+// ---- opt-in kernel timing (dit_profile_begin / dit_profile_end) ----
+struct ProfRec {
+  const char* name;
+  double flops, bytes;
+  hipEvent_t a, b;
+};
+struct Prof {
+  std::mutex mu;
+  bool on = false;
+  std::vector<ProfRec> recs;
+};
+Prof g_prof;
+
+template <class F>
+hipError_t timed(const char* name, double flops, double bytes, hipStream_t s, F&& launch) {
+  if (!g_prof.on) return launch();
+  hipEvent_t a, b;
+  hipError_t e = hipEventCreate(&a);
+  if (e != hipSuccess) return e;
+  if ((e = hipEventCreate(&b)) != hipSuccess) return e;
+  if ((e = hipEventRecord(a, s)) != hipSuccess) return e;
+  hipError_t le = launch();
+  if ((e = hipEventRecord(b, s)) != hipSuccess) return e;
+  std::lock_guard<std::mutex> g(g_prof.mu);
+  g_prof.recs.push_back(ProfRec{name, flops, bytes, a, b});
+  return le;
+}
+#define TIMED(name, flops, bytes, s, expr) HIP_TRY(timed(name, (double)(flops), (double)(bytes), s, [&]() { return (expr); }))
+
+double gemm_flops(const GemmPair& p) {
+  double f = 0;
+  for (int i = 0; i < p.nprob; i++) f += 2.0 * p.p[i].M * p.p[i].N * p.p[i].K;
+  return f;
+}
 
 inline size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
 inline bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
@@ -124,7 +162,7 @@ dit_status run_modulation(const dit_block_config* c, const dit_block_weights* w,
   const int D = c->hidden;
   float* silu = (float*)(ws + L.silu);
   float* mod = (float*)(ws + L.mod);
-  HIP_TRY(silu_f32(temb, silu, (int64_t)B * D, s));
+  TIMED("small_elementwise", 0, (double)B * D * 8, s, silu_f32(temb, silu, (int64_t)B * D, s));
   GemvArgs g{};
   for (int st = 0; st < 2; st++) {
     g.W[st] = w->mod_w[st];
@@ -138,7 +176,7 @@ dit_status run_modulation(const dit_block_config* c, const dit_block_weights* w,
   g.K = D;
   g.B = B;
   g.nstreams = 2;
-  HIP_TRY(gemv(g, c->dtype, s));
+  TIMED("mod_gemv", 2.0 * 2 * B * 6.0 * D * D, 2.0 * 6 * D * (double)D * esize(c->dtype), s, gemv(g, c->dtype, s));
   return DIT_OK;
 }
 
@@ -164,7 +202,7 @@ dit_status run_ln(const dit_block_config* c, int B, const void* x_img, const voi
   a.rows[1] = (int64_t)B * c->n_txt;
   a.D = D;
   a.eps = c->ln_eps;
-  HIP_TRY(ln_modulate(a, c->dtype, s));
+  TIMED("ln_modulate", 0, 2.0 * (a.rows[0] + a.rows[1]) * D * esize(c->dtype), s, ln_modulate(a, c->dtype, s));
   return DIT_OK;
 }
 
@@ -202,8 +240,8 @@ dit_status run_mlp_half(const dit_block_config* c, const dit_block_weights* w, i
     down.p[i].gate = mod + (size_t)i * B * 6 * D + 5 * D;
     down.p[i].gate_bstride = 6 * D;
   }
-  HIP_TRY(gemm(up, EPI_GELU, c->dtype, false, s));
-  HIP_TRY(gemm(down, EPI_RESID, c->dtype, false, s));
+  TIMED("gemm_mlp_up_gelu", gemm_flops(up), 0, s, gemm(up, EPI_GELU, c->dtype, false, s));
+  TIMED("gemm_mlp_down_gate", gemm_flops(down), 0, s, gemm(down, EPI_RESID, c->dtype, false, s));
   return DIT_OK;
 }
 
@@ -246,7 +284,7 @@ dit_status run_timestep(const dit_block_config* c, const dit_step_weights* w, in
   float* e = (float*)ws;
   float* h1 = (float*)(ws + al256((size_t)B * 256 * 4));
   float* s1 = (float*)(ws + al256((size_t)B * 256 * 4) + al256((size_t)B * D * 4));
-  HIP_TRY(timestep_sinusoid(t_dev, t, e, B, s));
+  TIMED("small_elementwise", 0, (double)B * 256 * 4, s, timestep_sinusoid(t_dev, t, e, B, s));
   GemvArgs g{};
   g.W[0] = w->t1_w;
   g.bias[0] = w->t1_b;
@@ -258,15 +296,15 @@ dit_status run_timestep(const dit_block_config* c, const dit_step_weights* w, in
   g.K = 256;
   g.B = B;
   g.nstreams = 1;
-  HIP_TRY(gemv(g, c->dtype, s));
-  HIP_TRY(silu_f32(h1, s1, (int64_t)B * D, s));
+  TIMED("timestep_gemv", 2.0 * B * D * 256, (double)D * 256 * esize(c->dtype), s, gemv(g, c->dtype, s));
+  TIMED("small_elementwise", 0, (double)B * D * 8, s, silu_f32(h1, s1, (int64_t)B * D, s));
   g.W[0] = w->t2_w;
   g.bias[0] = w->t2_b;
   g.out[0] = temb;
   g.in = s1;
   g.in_bstride = D;
   g.K = D;
-  HIP_TRY(gemv(g, c->dtype, s));
+  TIMED("timestep_gemv", 2.0 * B * D * D, (double)D * D * esize(c->dtype), s, gemv(g, c->dtype, s));
   return DIT_OK;
 }
 
@@ -276,13 +314,13 @@ dit_status run_patch(const dit_block_config* c, const dit_step_weights* w, int B
   const int M = B * c->n_img;
   const void* A = latent;
   if (c->dtype == DIT_BF16) {
-    HIP_TRY(cast_f32_to_bf16(latent, (u16*)ws, (int64_t)M * C, s));
+    TIMED("small_elementwise", 0, (double)M * C * 6, s, cast_f32_to_bf16(latent, (u16*)ws, (int64_t)M * C, s));
     A = ws;
   }
   GemmPair p{};
   p.nprob = 1;
   p.p[0] = problem(A, contiguous_rows(C), w->in_w, w->in_b, x_img, contiguous_rows(D), M, D, C);
-  HIP_TRY(gemm(p, EPI_STORE, c->dtype, false, s));
+  TIMED("gemm_patch_embed", gemm_flops(p), 0, s, gemm(p, EPI_STORE, c->dtype, false, s));
   return DIT_OK;
 }
 
@@ -292,7 +330,7 @@ dit_status run_final(const dit_block_config* c, const dit_step_weights* w, int B
   float* s1 = (float*)ws;
   float* fm = (float*)(ws + al256((size_t)B * D * 4));
   char* h = ws + al256((size_t)B * D * 4) + al256((size_t)B * 2 * D * 4);
-  HIP_TRY(silu_f32(temb, s1, (int64_t)B * D, s));
+  TIMED("small_elementwise", 0, (double)B * D * 8, s, silu_f32(temb, s1, (int64_t)B * D, s));
   GemvArgs g{};
   g.W[0] = w->fmod_w;
   g.bias[0] = w->fmod_b;
@@ -304,7 +342,7 @@ dit_status run_final(const dit_block_config* c, const dit_step_weights* w, int B
   g.K = D;
   g.B = B;
   g.nstreams = 1;
-  HIP_TRY(gemv(g, c->dtype, s));
+  TIMED("final_gemv", 2.0 * B * 2 * D * D, 2.0 * D * D * esize(c->dtype), s, gemv(g, c->dtype, s));
   LnArgs a{};
   a.x[0] = x_img;
   a.xmap[0] = stream_rows(c->n_img, D);
@@ -318,11 +356,11 @@ dit_status run_final(const dit_block_config* c, const dit_step_weights* w, int B
   a.rows[1] = 0;
   a.D = D;
   a.eps = c->ln_eps;
-  HIP_TRY(ln_modulate(a, c->dtype, s));
+  TIMED("ln_modulate", 0, 2.0 * a.rows[0] * D * esize(c->dtype), s, ln_modulate(a, c->dtype, s));
   GemmPair p{};
   p.nprob = 1;
   p.p[0] = problem(h, contiguous_rows(D), w->fout_w, w->fout_b, v, contiguous_rows(C), B * c->n_img, C, D);
-  HIP_TRY(gemm(p, EPI_STORE, c->dtype, true, s));
+  TIMED("gemm_final", gemm_flops(p), 0, s, gemm(p, EPI_STORE, c->dtype, true, s));
   return DIT_OK;
 }
 
@@ -396,7 +434,7 @@ dit_status dit_block_forward(const dit_block_config* c, const dit_block_weights*
   float* rope = (float*)(ws + L.rope);
 
   if ((st = run_modulation(c, w, B, temb, ws, L, s))) return st;
-  if (c->rope) HIP_TRY(rope_table(rope, std::max(c->grid_h, c->grid_w), d, c->rope_theta, s));
+  if (c->rope) TIMED("small_elementwise", 0, 0, s, rope_table(rope, std::max(c->grid_h, c->grid_w), d, c->rope_theta, s));
   // pre-attention LN + modulate into h
   if ((st = run_ln(c, B, x_img, x_txt, ws, L, 0, D, s))) return st;
   // QKV projection straight into the joint [B][S][3][H][d] buffer (+ RoPE on image q, k)
@@ -410,7 +448,7 @@ dit_status dit_block_forward(const dit_block_config* c, const dit_block_weights*
     qkv.p[i].grid_w = c->grid_w;
   }
   if (c->rope) qkv.p[0].rope_tab = rope;
-  HIP_TRY(gemm(qkv, EPI_QKV, c->dtype, false, s));
+  TIMED("gemm_qkv_rope", gemm_flops(qkv), 0, s, gemm(qkv, EPI_QKV, c->dtype, false, s));
   // joint attention over [text ; image]; output o reuses the h buffer
   AttnArgs at{};
   char* qkvp = ws + L.qkv;
@@ -430,7 +468,7 @@ dit_status dit_block_forward(const dit_block_config* c, const dit_block_weights*
   at.os_s = D;
   at.os_h = d;
   at.scale = 1.0f / std::sqrt((float)d);
-  HIP_TRY(attention(at, c->dtype, s));
+  TIMED("attention", 4.0 * B * H * (double)S * S * d, 0, s, attention(at, c->dtype, s));
   // output projection + gate1 residual, in place on x
   GemmPair proj{};
   proj.nprob = 2;
@@ -440,7 +478,7 @@ dit_status dit_block_forward(const dit_block_config* c, const dit_block_weights*
     proj.p[i].gate = mod + (size_t)i * B * 6 * D + 2 * D;
     proj.p[i].gate_bstride = 6 * D;
   }
-  HIP_TRY(gemm(proj, EPI_RESID, c->dtype, false, s));
+  TIMED("gemm_out_gate", gemm_flops(proj), 0, s, gemm(proj, EPI_RESID, c->dtype, false, s));
   return run_mlp_half(c, w, B, x_img, x_txt, ws, L, s);
 }
 
@@ -487,7 +525,7 @@ dit_status joint_attention(const void* q, const void* k, const void* v, void* o,
   a.os_s = o_stride_s;
   a.os_h = o_stride_h;
   a.scale = scale;
-  HIP_TRY(attention(a, dtype, hs(stream)));
+  TIMED("attention", 4.0 * batch * heads * (double)seq * seq * head_dim, 0, hs(stream), attention(a, dtype, hs(stream)));
   return DIT_OK;
 }
 
@@ -499,7 +537,7 @@ dit_status flow_step(float* x, const float* v, const float* noise, int64_t n, fl
   if (st) return st;
   if (n == 0) return DIT_OK;
   if (!x || !v) return fail(DIT_ERR_INVALID_ARG, "x/v NULL");
-  HIP_TRY(flow_update(x, v, noise_level > 0.f ? noise : nullptr, n, cx, cv, ce, hs(stream)));
+  TIMED("flow_step", 0, (noise_level > 0.f ? 16.0 : 12.0) * n, hs(stream), flow_update(x, v, noise_level > 0.f ? noise : nullptr, n, cx, cv, ce, hs(stream)));
   return DIT_OK;
 }
 
@@ -519,7 +557,7 @@ dit_status group_reward_stats(const float* rewards, int32_t groups, int32_t n, f
   HIP_TRY(hipStreamSynchronize(s));
   for (size_t i = 0; i < host.size(); i++)
     if (!std::isfinite(host[i])) return fail(DIT_ERR_NAN, "reward %zu (group %zu) is not finite", i % n, i / n);
-  HIP_TRY(reward_stats(rewards, groups, n, adv_eps, k_select, mean, stdv, adv, order, selected, s));
+  TIMED("reward_stats", 0, 4.0 * groups * n, s, reward_stats(rewards, groups, n, adv_eps, k_select, mean, stdv, adv, order, selected, s));
   return DIT_OK;
 }
 
@@ -602,8 +640,55 @@ dit_status dit_denoise_step(const dit_block_config* c, const dit_step_weights* s
   for (int i = 0; i < n_blocks; i++)
     if ((st = dit_block_forward(c, &blocks[i], B, temb, ximg, xtxt, inner, inner_bytes, stream))) return st;
   if ((st = run_final(c, sw, B, C, temb, ximg, v, inner, s))) return st;
-  HIP_TRY(flow_update(latent, v, noise_level > 0.f ? noise : nullptr, (int64_t)B * c->n_img * C, cx, cv, ce, s));
+  TIMED("flow_step", 0, (noise_level > 0.f ? 16.0 : 12.0) * B * c->n_img * C, s,
+        flow_update(latent, v, noise_level > 0.f ? noise : nullptr, (int64_t)B * c->n_img * C, cx, cv, ce, s));
   return DIT_OK;
+}
+
+dit_status dit_profile_begin(void) {
+  std::lock_guard<std::mutex> g(g_prof.mu);
+  for (auto& r : g_prof.recs) {
+    (void)hipEventDestroy(r.a);
+    (void)hipEventDestroy(r.b);
+  }
+  g_prof.recs.clear();
+  g_prof.on = true;
+  return DIT_OK;
+}
+
+dit_status dit_profile_end(dit_kernel_stat* stats, int32_t capacity, int32_t* count) {
+  std::lock_guard<std::mutex> g(g_prof.mu);
+  g_prof.on = false;
+  std::map<std::string, dit_kernel_stat> agg;
+  std::vector<std::string> order;
+  dit_status st = DIT_OK;
+  for (auto& r : g_prof.recs) {
+    float ms = 0.f;
+    hipError_t e = hipEventSynchronize(r.b);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, r.a, r.b);
+    if (e != hipSuccess && st == DIT_OK) st = fail(DIT_ERR_HIP, "event timing failed: %s", hipGetErrorString(e));
+    auto it = agg.find(r.name);
+    if (it == agg.end()) {
+      dit_kernel_stat k{};
+      std::strncpy(k.name, r.name, sizeof(k.name) - 1);
+      it = agg.emplace(r.name, k).first;
+      order.push_back(r.name);
+    }
+    it->second.launches += 1;
+    it->second.total_ms += ms;
+    it->second.flops += r.flops;
+    it->second.bytes += r.bytes;
+    (void)hipEventDestroy(r.a);
+    (void)hipEventDestroy(r.b);
+  }
+  g_prof.recs.clear();
+  int32_t n = 0;
+  for (auto& name : order) {
+    if (stats && n < capacity) stats[n] = agg[name];
+    n++;
+  }
+  if (count) *count = n;
+  return st;
 }
 
 }  // extern "C"

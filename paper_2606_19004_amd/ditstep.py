@@ -28,7 +28,7 @@ STATUS = {0: "DIT_OK", 1: "DIT_ERR_INVALID_ARG", 2: "DIT_ERR_SHAPE", 3: "DIT_ERR
 EXPORTS = ("dit_abi_version", "dit_status_string", "dit_last_error_message", "dit_block_workspace_bytes",
            "dit_block_forward", "dit_block_mlp", "joint_attention", "flow_step", "group_reward_stats",
            "dit_timestep_embed", "dit_patch_embed", "dit_final_layer", "dit_denoise_workspace_bytes",
-           "dit_denoise_step")
+           "dit_denoise_step", "dit_profile_begin", "dit_profile_end")
 
 
 class DitError(RuntimeError):
@@ -57,6 +57,11 @@ class StepWeights(C.Structure):
     _fields_ = [(n, C.c_void_p) for n in _STEP_TENSORS]
 
 
+class KernelStat(C.Structure):
+    _fields_ = [("name", C.c_char * 40), ("launches", C.c_int32), ("total_ms", C.c_double),
+                ("flops", C.c_double), ("bytes", C.c_double)]
+
+
 _stream = C.c_void_p
 _i32, _i64, _f32, _sz = C.c_int32, C.c_int64, C.c_float, C.c_size_t
 _vp = C.c_void_p
@@ -78,6 +83,8 @@ _sigs = {
     "dit_denoise_workspace_bytes": ([C.POINTER(BlockConfig), _i32, _i32], _sz),
     "dit_denoise_step": ([C.POINTER(BlockConfig), C.POINTER(StepWeights), C.POINTER(BlockWeights), _i32, _i32, _i32,
                           _f32, _f32, _f32, _vp, _vp, _vp, _vp, _vp, _sz, _stream], _i32),
+    "dit_profile_begin": ([], _i32),
+    "dit_profile_end": ([C.POINTER(KernelStat), _i32, C.POINTER(_i32)], _i32),
 }
 for _name, (_args, _res) in _sigs.items():
     _fn = getattr(_lib, _name)
@@ -206,3 +213,17 @@ def dit_denoise_step(cfg, sw, blocks, t, t_next, noise_level, latent, x_txt, noi
     _check(_lib.dit_denoise_step(C.byref(cfg), C.byref(sw), arr, len(blocks), latent.shape[0], latent.shape[-1],
                                  t, t_next, noise_level, _ptr(latent), _ptr(x_txt), _ptr(noise), _ptr(v_out),
                                  _ptr(ws), ws.numel(), _s(stream)))
+
+
+def dit_profile_begin():
+    _check(_lib.dit_profile_begin())
+
+
+def dit_profile_end() -> list:
+    """Per-kernel-class totals since dit_profile_begin: list of dicts (name, launches, total_ms, flops, bytes)."""
+    cap = 64
+    arr = (KernelStat * cap)()
+    n = _i32(0)
+    _check(_lib.dit_profile_end(arr, cap, C.byref(n)))
+    return [{"name": arr[i].name.decode(), "launches": arr[i].launches, "total_ms": arr[i].total_ms,
+             "flops": arr[i].flops, "bytes": arr[i].bytes} for i in range(min(n.value, cap))]

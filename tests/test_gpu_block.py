@@ -127,7 +127,8 @@ def test_block_errors_write_nothing(d):
     with pytest.raises(d.DitError) as ei:
         d.dit_block_forward(c, bw, temb, xi, xt, d.workspace(need - 256))
     assert ei.value.name == "DIT_ERR_WORKSPACE"
-    bad = block_cfg(d, dataclasses.replace(cfg, grid_w=cfg.grid_w + 1))
+    bad = d.block_config(cfg.hidden, cfg.heads, cfg.head_dim, cfg.mlp_hidden, cfg.n_img + 1, cfg.n_txt,
+                         cfg.grid_h, cfg.grid_w)                     # n_img != grid_h * grid_w
     with pytest.raises(d.DitError) as ei:
         d.dit_block_forward(bad, bw, temb, xi, xt, d.workspace(need))
     assert ei.value.name == "DIT_ERR_SHAPE"
