@@ -103,8 +103,10 @@ dit_status check_ws(void* ws, size_t have, size_t need) {
 
 // offsets into the block workspace
 struct BlockWs {
-  size_t mod, silu, rope, h, qkv, u, total;
+  size_t mod, silu, xs, rope, h, qkv, u, total;
 };
+// scratch of the MFMA GEMV: 16 samples x K, as bf16 hi and lo parts
+inline size_t xs_bytes(int64_t K) { return al256(2 * 16 * (size_t)K * 2); }
 BlockWs block_layout(const dit_block_config* c, int64_t B) {
   BlockWs w;
   size_t es = esize(c->dtype);
@@ -113,6 +115,7 @@ BlockWs block_layout(const dit_block_config* c, int64_t B) {
   size_t off = 0;
   w.mod = off;  off += al256(2 * B * 6 * D * 4);
   w.silu = off; off += al256(B * D * 4);
+  w.xs = off;   off += xs_bytes(std::max<size_t>(D, 256));
   w.rope = off; off += al256(npos * (c->head_dim / 4) * 2 * 4);
   w.h = off;    off += al256(B * S * D * es);
   w.qkv = off;  off += al256(B * S * 3 * D * es);
@@ -156,13 +159,29 @@ RowMap joint_rows(const dit_block_config* c, int stream, int64_t cols) {
 }
 RowMap stream_rows(int64_t n, int64_t cols) { return RowMap{std::max<int64_t>(n, 1), n * cols, cols, 0}; }
 
+// out = W act(in) + b with act = SiLU when silu_in: MFMA (hi/lo split) for bf16
+// weights, VALU for fp32 weights (which first writes SiLU(in) to silu_buf)
+dit_status run_gemv(const dit_block_config* c, GemvArgs g, bool silu_in, float* silu_buf, void* xs,
+                    const char* name, hipStream_t s) {
+  double flops = 2.0 * g.nstreams * g.B * (double)g.N * g.K;
+  double bytes = (double)g.nstreams * g.N * (double)g.K * esize(c->dtype);
+  if (c->dtype == DIT_BF16) {
+    TIMED(name, flops, bytes, s, gemv_bf16(g, (u16*)xs, silu_in ? 1 : 0, s));
+    return DIT_OK;
+  }
+  if (silu_in) {
+    TIMED("small_elementwise", 0, (double)g.B * g.K * 8, s, silu_f32(g.in, silu_buf, (int64_t)g.B * g.in_bstride, s));
+    g.in = silu_buf;
+  }
+  TIMED(name, flops, bytes, s, gemv(g, c->dtype, s));
+  return DIT_OK;
+}
+
 // mod[s][b][6D] = W_mod[s] SiLU(temb[b]) + b_mod[s]
 dit_status run_modulation(const dit_block_config* c, const dit_block_weights* w, int B, const float* temb,
                           char* ws, const BlockWs& L, hipStream_t s) {
   const int D = c->hidden;
-  float* silu = (float*)(ws + L.silu);
   float* mod = (float*)(ws + L.mod);
-  TIMED("small_elementwise", 0, (double)B * D * 8, s, silu_f32(temb, silu, (int64_t)B * D, s));
   GemvArgs g{};
   for (int st = 0; st < 2; st++) {
     g.W[st] = w->mod_w[st];
@@ -170,14 +189,13 @@ dit_status run_modulation(const dit_block_config* c, const dit_block_weights* w,
     g.out[st] = mod + (size_t)st * B * 6 * D;
   }
   g.out_bstride = 6 * D;
-  g.in = silu;
+  g.in = temb;
   g.in_bstride = D;
   g.N = 6 * D;
   g.K = D;
   g.B = B;
   g.nstreams = 2;
-  TIMED("mod_gemv", 2.0 * 2 * B * 6.0 * D * D, 2.0 * 6 * D * (double)D * esize(c->dtype), s, gemv(g, c->dtype, s));
-  return DIT_OK;
+  return run_gemv(c, g, true, (float*)(ws + L.silu), ws + L.xs, "mod_gemv", s);
 }
 
 // h = LN(x)(1+scale)+shift for both streams into the joint [B][S][D] buffer
@@ -249,12 +267,15 @@ struct StepWs {
   size_t temb, ximg, xtxt, v, inner, total;
 };
 
-size_t timestep_ws(const dit_block_config* c, int64_t B) { return al256(B * 256 * 4) + 2 * al256(B * c->hidden * 4); }
+size_t timestep_ws(const dit_block_config* c, int64_t B) {
+  return al256(B * 256 * 4) + 2 * al256(B * c->hidden * 4) + xs_bytes(std::max(c->hidden, 256));
+}
 size_t patch_ws(const dit_block_config* c, int64_t B, int C) {
   return c->dtype == DIT_BF16 ? al256(B * c->n_img * C * 2) : 0;
 }
 size_t final_ws(const dit_block_config* c, int64_t B) {
-  return al256(B * c->hidden * 4) + al256(B * 2 * c->hidden * 4) + al256(B * c->n_img * c->hidden * esize(c->dtype));
+  return al256(B * c->hidden * 4) + al256(B * 2 * c->hidden * 4) + al256(B * c->n_img * c->hidden * esize(c->dtype)) +
+         xs_bytes(c->hidden);
 }
 
 StepWs step_layout(const dit_block_config* c, int64_t B, int C) {
@@ -284,6 +305,7 @@ dit_status run_timestep(const dit_block_config* c, const dit_step_weights* w, in
   float* e = (float*)ws;
   float* h1 = (float*)(ws + al256((size_t)B * 256 * 4));
   float* s1 = (float*)(ws + al256((size_t)B * 256 * 4) + al256((size_t)B * D * 4));
+  char* xs = ws + al256((size_t)B * 256 * 4) + 2 * al256((size_t)B * D * 4);
   TIMED("small_elementwise", 0, (double)B * 256 * 4, s, timestep_sinusoid(t_dev, t, e, B, s));
   GemvArgs g{};
   g.W[0] = w->t1_w;
@@ -296,16 +318,15 @@ dit_status run_timestep(const dit_block_config* c, const dit_step_weights* w, in
   g.K = 256;
   g.B = B;
   g.nstreams = 1;
-  TIMED("timestep_gemv", 2.0 * B * D * 256, (double)D * 256 * esize(c->dtype), s, gemv(g, c->dtype, s));
-  TIMED("small_elementwise", 0, (double)B * D * 8, s, silu_f32(h1, s1, (int64_t)B * D, s));
+  dit_status st = run_gemv(c, g, false, nullptr, xs, "timestep_gemv", s);
+  if (st) return st;
   g.W[0] = w->t2_w;
   g.bias[0] = w->t2_b;
   g.out[0] = temb;
-  g.in = s1;
+  g.in = h1;
   g.in_bstride = D;
   g.K = D;
-  TIMED("timestep_gemv", 2.0 * B * D * D, (double)D * D * esize(c->dtype), s, gemv(g, c->dtype, s));
-  return DIT_OK;
+  return run_gemv(c, g, true, s1, xs, "timestep_gemv", s);
 }
 
 dit_status run_patch(const dit_block_config* c, const dit_step_weights* w, int B, int C, const float* latent,
@@ -330,19 +351,20 @@ dit_status run_final(const dit_block_config* c, const dit_step_weights* w, int B
   float* s1 = (float*)ws;
   float* fm = (float*)(ws + al256((size_t)B * D * 4));
   char* h = ws + al256((size_t)B * D * 4) + al256((size_t)B * 2 * D * 4);
-  TIMED("small_elementwise", 0, (double)B * D * 8, s, silu_f32(temb, s1, (int64_t)B * D, s));
+  char* xs = h + al256((size_t)B * c->n_img * D * esize(c->dtype));
   GemvArgs g{};
   g.W[0] = w->fmod_w;
   g.bias[0] = w->fmod_b;
   g.out[0] = fm;
   g.out_bstride = 2 * D;
-  g.in = s1;
+  g.in = temb;
   g.in_bstride = D;
   g.N = 2 * D;
   g.K = D;
   g.B = B;
   g.nstreams = 1;
-  TIMED("final_gemv", 2.0 * B * 2 * D * D, 2.0 * D * D * esize(c->dtype), s, gemv(g, c->dtype, s));
+  dit_status st = run_gemv(c, g, true, s1, xs, "final_gemv", s);
+  if (st) return st;
   LnArgs a{};
   a.x[0] = x_img;
   a.xmap[0] = stream_rows(c->n_img, D);

@@ -104,7 +104,10 @@ struct GemvArgs {
   const float* in; int64_t in_bstride;
   int N, K, B, nstreams;
 };
-hipError_t gemv(const GemvArgs& a, int dtype, hipStream_t s);
+hipError_t gemv(const GemvArgs& a, int dtype, hipStream_t s);   // VALU (fp32 weights)
+// bf16 weights through MFMA; xs = scratch [2][16][K] bf16; silu_in applies SiLU to the input first;
+// K must be a multiple of 32
+hipError_t gemv_bf16(const GemvArgs& a, u16* xs, int silu_in, hipStream_t s);
 
 hipError_t silu_f32(const float* in, float* out, int64_t n, hipStream_t s);
 hipError_t cast_f32_to_bf16(const float* in, u16* out, int64_t n, hipStream_t s);

@@ -300,6 +300,92 @@ __global__ void __launch_bounds__(256) gemv_kernel(GemvArgs a, int b0, int nb) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// bf16 weights: an MFMA skinny GEMM. The fp32 input (at most 16 samples per
+// pass) is split once into bf16 hi + lo parts (x = hi + lo to ~2^-16), laid out
+// [2][16][K]; each wave then streams 32 weight rows once and multiplies them
+// against both parts with v_mfma_f32_16x16x32_bf16 (samples are the MFMA's
+// 16-wide N dimension), so HBM bandwidth, not VALU FMAs, sets the time.
+// ---------------------------------------------------------------------------
+__global__ void split_hilo_kernel(const float* __restrict__ in, int64_t stride, int b0, int nb, int K, int silu,
+                                  u16* __restrict__ out) {
+  int k = blockIdx.x * 256 + threadIdx.x, b = blockIdx.y;
+  if (k >= K) return;
+  float x = 0.f;
+  if (b < nb) {
+    x = in[(int64_t)(b0 + b) * stride + k];
+    if (silu) x = x / (1.0f + __expf(-x));
+  }
+  __bf16 hi = (__bf16)x;
+  __bf16 lo = (__bf16)(x - (float)hi);
+  out[(int64_t)b * K + k] = __builtin_bit_cast(u16, hi);
+  out[(int64_t)(16 + b) * K + k] = __builtin_bit_cast(u16, lo);
+}
+
+__global__ void __launch_bounds__(256) gemv_mfma_kernel(GemvArgs a, const u16* __restrict__ xs, int b0, int nb) {
+  const int s = blockIdx.y;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int n0 = blockIdx.x * 128 + wave * 32;
+  if (n0 >= a.N) return;
+  const int K = a.K;
+  const int r16 = lane & 15, kq = (lane >> 4) * 8;
+  // operand A: rows n0 + r16 and n0 + 16 + r16 (clamped; results of clamped rows are dropped)
+  const u16* W = (const u16*)a.W[s];
+  const u16* w0 = W + (int64_t)min(n0 + r16, a.N - 1) * K + kq;
+  const u16* w1 = W + (int64_t)min(n0 + 16 + r16, a.N - 1) * K + kq;
+  // operand B: sample r16, hi and lo parts
+  const u16* xh = xs + (int64_t)r16 * K + kq;
+  const u16* xl = xs + (int64_t)(16 + r16) * K + kq;
+  f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+  int k = 0;
+  for (; k + 128 <= K; k += 128) {
+    bf16x8 fa[4], fb[4], fh[4], fl[4];
+#pragma unroll
+    for (int u = 0; u < 4; u++) {
+      fa[u] = *(const bf16x8*)(w0 + k + 32 * u);
+      fb[u] = *(const bf16x8*)(w1 + k + 32 * u);
+      fh[u] = *(const bf16x8*)(xh + k + 32 * u);
+      fl[u] = *(const bf16x8*)(xl + k + 32 * u);
+    }
+#pragma unroll
+    for (int u = 0; u < 4; u++) {
+      acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[u], fh[u], acc0, 0, 0, 0);
+      acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[u], fl[u], acc0, 0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[u], fh[u], acc1, 0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[u], fl[u], acc1, 0, 0, 0);
+    }
+  }
+  for (; k < K; k += 32) {
+    bf16x8 fa = *(const bf16x8*)(w0 + k), fb = *(const bf16x8*)(w1 + k);
+    bf16x8 fh = *(const bf16x8*)(xh + k), fl = *(const bf16x8*)(xl + k);
+    acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa, fh, acc0, 0, 0, 0);
+    acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa, fl, acc0, 0, 0, 0);
+    acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb, fh, acc1, 0, 0, 0);
+    acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb, fl, acc1, 0, 0, 0);
+  }
+  // accumulator register r of lane l: weight row 4 (l / 16) + r, sample l % 16
+  const int b = lane & 15;
+  if (b >= nb) return;
+  const u16* bias = (const u16*)a.bias[s];
+  float* out = a.out[s] + (int64_t)(b0 + b) * a.out_bstride;
+#pragma unroll
+  for (int r = 0; r < 4; r++) {
+    int n = n0 + 4 * (lane >> 4) + r;
+    if (n < a.N) out[n] = acc0[r] + (bias ? to_f32(bias[n]) : 0.f);
+    if (n + 16 < a.N) out[n + 16] = acc1[r] + (bias ? to_f32(bias[n + 16]) : 0.f);
+  }
+}
+
+hipError_t gemv_bf16(const GemvArgs& a, u16* xs, int silu_in, hipStream_t s) {
+  if (a.N == 0 || a.B == 0) return hipSuccess;
+  for (int b0 = 0; b0 < a.B; b0 += 16) {
+    int nb = std::min(16, a.B - b0);
+    split_hilo_kernel<<<dim3(cdiv(a.K, 256), 16), 256, 0, s>>>(a.in, a.in_bstride, b0, nb, a.K, silu_in, xs);
+    gemv_mfma_kernel<<<dim3(cdiv(a.N, 128), a.nstreams), 256, 0, s>>>(a, xs, b0, nb);
+  }
+  return hipGetLastError();
+}
+
 template <typename T>
 static hipError_t gemv_launch(const GemvArgs& a, hipStream_t s) {
   dim3 grid(cdiv(a.N, 16), a.nstreams);

@@ -10,8 +10,12 @@
 //     staging), double-buffered. Out-of-range rows use an offset past the
 //     buffer's num_records, which the hardware turns into zeros.
 //   * LDS rows are 64 bf16 = 8 chunks of 16 bytes; chunk c of row r is stored
-//     at chunk slot c ^ (r % 8), so the 8 lanes of a ds_read_b128 phase hit 8
-//     different bank groups.
+//     at slot c ^ ((r ^ r >> 3) & 7), so the 16 lanes of a ds_read_b128 cycle
+//     hit 16 different bank groups of the 64-bank LDS.
+//   * The large tile (256 x 256) runs 8 waves (2 per SIMD), each 64 rows x 128
+//     features; fragments of the next 16-deep k step load while the current
+//     step's MFMAs run, and a k-tile barrier sits at the last step so it
+//     overlaps MFMAs in flight.
 //   * Workgroups are dispatched round-robin over the 8 XCDs; tile t is given
 //     to workgroup ids so that each XCD owns one contiguous range of tiles,
 //     ordered in groups of 8 M-tiles so concurrently running tiles share A and
@@ -53,8 +57,26 @@ template <> __device__ __forceinline__ void store4<float>(float* p, const float*
   *(float4*)p = make_float4(f[0], f[1], f[2], f[3]);
 }
 
+// Per-row epilogue state, computed once per output row m.
+struct RowEpi {
+  int64_t off;   // element offset of row m in C
+  int64_t gate;  // element offset of the row's gate vector (EPI_RESID)
+  int rpos, cpos;  // grid row / column of an image token (EPI_QKV with RoPE)
+};
+
+__device__ __forceinline__ RowEpi row_epi(const GemmProblem& P, int m) {
+  RowEpi r;
+  int rpb = (int)P.cmap.rows_per_batch;
+  int b = m / rpb, i = m - b * rpb;
+  r.off = (int64_t)b * P.cmap.batch_stride + (int64_t)i * P.cmap.row_stride + P.cmap.offset;
+  r.gate = (int64_t)b * P.gate_bstride;
+  r.rpos = P.grid_w > 0 ? i / P.grid_w : 0;
+  r.cpos = P.grid_w > 0 ? i - r.rpos * P.grid_w : 0;
+  return r;
+}
+
 template <int EPI, typename TW, typename TC>
-__device__ __forceinline__ void epilogue4(const GemmProblem& P, int m, int n, float* v) {
+__device__ __forceinline__ void epilogue4(const GemmProblem& P, const RowEpi& R, int n, float* v) {
   if (P.bias) {
     float b[4];
     load4<TW>((const TW*)P.bias + n, b);
@@ -65,10 +87,9 @@ __device__ __forceinline__ void epilogue4(const GemmProblem& P, int m, int n, fl
 #pragma unroll
     for (int q = 0; q < 4; q++) v[q] = gelu_tanh_f(v[q]);
   }
-  TC* out = (TC*)P.C + row_offset(P.cmap, m) + n;
+  TC* out = (TC*)P.C + R.off + n;
   if (EPI == EPI_RESID) {
-    int64_t b = m / P.cmap.rows_per_batch;
-    float4 g = *(const float4*)(P.gate + b * P.gate_bstride + n);
+    float4 g = *(const float4*)(P.gate + R.gate + n);
     float x[4];
     load4<TC>(out, x);
     v[0] = fmaf(g.x, v[0], x[0]);
@@ -78,15 +99,13 @@ __device__ __forceinline__ void epilogue4(const GemmProblem& P, int m, int n, fl
   }
   if (EPI == EPI_QKV) {
     if (P.rope_tab && n < 2 * P.hidden) {
-      // image token i = m % rows_per_batch at grid (i / grid_w, i % grid_w);
-      // head dims [0, d/2) rotate by the row, [d/2, d) by the column
-      int i = (int)(m % P.cmap.rows_per_batch);
-      int dd = n % P.head_dim;
-      int half = P.head_dim >> 1;
-      int pos = dd < half ? i / P.grid_w : i % P.grid_w;
-      int pr = (dd % half) >> 1;   // pair index of (dd, dd+1)
-      const float* cs = P.rope_tab + ((int64_t)pos * (P.head_dim >> 2) + pr) * 2;
-      float4 t = *(const float4*)cs;   // pairs pr and pr+1
+      // head dims [0, d/2) rotate by the token's grid row, [d/2, d) by its column;
+      // n..n+3 hold the pairs (pr, pr+1) of one half (head_dim is a power of two)
+      int dd = n & (P.head_dim - 1);
+      int hh = P.head_dim >> 1;
+      int pos = dd < hh ? R.rpos : R.cpos;
+      int pr = (dd & (hh - 1)) >> 1;
+      float4 t = *(const float4*)(P.rope_tab + ((int64_t)pos * (P.head_dim >> 2) + pr) * 2);
       float a0 = v[0], b0 = v[1], a1 = v[2], b1 = v[3];
       v[0] = a0 * t.x - b0 * t.y;
       v[1] = a0 * t.y + b0 * t.x;
@@ -113,14 +132,20 @@ __device__ __forceinline__ void tile_coords(int tl, int mt, int nt, int& tm, int
   tn = in_group / gm;
 }
 
+// LDS swizzle key of tile row r: chunk c of row r lives in slot c ^ f(r). Any 16
+// consecutive rows read at one chunk hit 16 distinct 16-byte bank groups (the
+// 64-bank LDS serves 16 lanes of a ds_read_b128 per cycle).
+__device__ __forceinline__ int swz(int r) { return (r ^ (r >> 3)) & 7; }
+
 template <int BM, int BN, int WM, int WN, int EPI, bool OUTF32>
-__global__ void __launch_bounds__(256) gemm_bf16_kernel(GemmPair pr, int tiles0, int total_tiles) {
+__global__ void __launch_bounds__(WM * WN * 64) gemm_bf16_kernel(GemmPair pr, int tiles0, int total_tiles) {
+  constexpr int NW = WM * WN;
   constexpr int BK = 64;
-  constexpr int WTM = BM / WM, WTN = BN / WN;  // wave tile (m, n)
-  constexpr int TJ = WTM / 32, TI = WTN / 32;  // 32x32 MFMA blocks per wave along m and n
-  constexpr int A_LOADS = BM / 32, W_LOADS = BN / 32;  // 8-row groups loaded per wave per k-tile
+  constexpr int WTM = BM / WM, WTN = BN / WN;          // wave tile (m, n)
+  constexpr int TJ = WTM / 32, TI = WTN / 32;          // 32x32 MFMA blocks per wave along m and n
+  constexpr int A_LOADS = BM / 8 / NW, W_LOADS = BN / 8 / NW;  // 8-row groups each wave loads per k-tile
   constexpr int A_BYTES = BM * BK * 2, W_BYTES = BN * BK * 2;
-  static_assert(WM * WN == 4, "four waves");
+  static_assert(A_LOADS >= 1 && W_LOADS >= 1, "every wave loads at least one row group");
 #if defined(__HIP_DEVICE_COMPILE__)  // the buffer-resource builtins exist only in the device pass
   extern __shared__ __attribute__((aligned(1024))) char smem[];
 
@@ -143,20 +168,23 @@ __global__ void __launch_bounds__(256) gemm_bf16_kernel(GemmPair pr, int tiles0,
   const uint32_t OOB = 0x80000000u;
   __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc((void*)P.A, (short)0, 0x7fffffff, 0x00020000);
   __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc((void*)P.W, (short)0, 0x7fffffff, 0x00020000);
-  const int lrow = lane >> 3;                    // row inside an 8-row group
-  const int lchunk = (lane & 7) ^ lrow;          // global chunk this lane fetches (slot = lane & 7)
+  // a wave-load writes 8 rows x 8 slots (lane -> row lane/8, slot lane%8) and fetches chunk slot ^ f(row)
+  const int lrow = lane >> 3;
   uint32_t aoff[A_LOADS], woff[W_LOADS];
 #pragma unroll
   for (int i = 0; i < A_LOADS; i++) {
-    int m = m0 + (wave * A_LOADS + i) * 8 + lrow;
-    aoff[i] = m < P.M ? (uint32_t)(row_offset(P.amap, m) * 2 + lchunk * 16) : OOB;
+    int g = wave * A_LOADS + i;
+    int chunk = (lane & 7) ^ swz(8 * g + lrow);
+    int m = m0 + 8 * g + lrow;
+    aoff[i] = m < P.M ? (uint32_t)(row_offset(P.amap, m) * 2 + chunk * 16) : OOB;
   }
 #pragma unroll
   for (int i = 0; i < W_LOADS; i++) {
-    int n = n0 + (wave * W_LOADS + i) * 8 + lrow;
-    woff[i] = n < P.N ? (uint32_t)((int64_t)n * K * 2 + lchunk * 16) : OOB;
+    int g = wave * W_LOADS + i;
+    int chunk = (lane & 7) ^ swz(8 * g + lrow);
+    int n = n0 + 8 * g + lrow;
+    woff[i] = n < P.N ? (uint32_t)((int64_t)n * K * 2 + chunk * 16) : OOB;
   }
-
   auto issue = [&](int kt, int buf) {
     char* sa = smem + buf * (A_BYTES + W_BYTES);
     char* sw = sa + A_BYTES;
@@ -178,44 +206,74 @@ __global__ void __launch_bounds__(256) gemm_bf16_kernel(GemmPair pr, int tiles0,
       for (int r = 0; r < 16; r++) acc[i][j][r] = 0.f;
 
   const int wm = wave / WN, wn = wave % WN;
-  const int half = lane >> 5, l32 = lane & 31, sw8 = lane & 7;
+  const int half = lane >> 5, l32 = lane & 31;
   const int nk = K / BK;
-  issue(0, 0);
-  for (int kt = 0; kt < nk; kt++) {
-    __builtin_amdgcn_s_waitcnt(0);   // this wave's loads of tile kt have landed in LDS
-    __syncthreads();                 // ... and everyone's; the other buffer is free again
-    if (kt + 1 < nk) issue(kt + 1, (kt + 1) & 1);
-    const char* sa = smem + (kt & 1) * (A_BYTES + W_BYTES);
+  int fwk[TI], fak[TJ];
+#pragma unroll
+  for (int i = 0; i < TI; i++) fwk[i] = swz(wn * WTN + 32 * i + l32);
+#pragma unroll
+  for (int j = 0; j < TJ; j++) fak[j] = swz(wm * WTM + 32 * j + l32);
+  const int wrow0 = (wn * WTN + l32) * 128, arow0 = (wm * WTM + l32) * 128;
+  // fragments of k16 step s, register-double-buffered so step s+1 loads while step s multiplies
+  bf16x8 fw[2][TI], fa[2][TJ];
+  auto frags = [&](int buf, int s, int rb) {
+    const char* sa = smem + buf * (A_BYTES + W_BYTES);
     const char* sw = sa + A_BYTES;
+    const int c = 2 * s + half;
+#pragma unroll
+    for (int i = 0; i < TI; i++) fw[rb][i] = *(const bf16x8*)(sw + wrow0 + 32 * i * 128 + ((c ^ fwk[i]) << 4));
+#pragma unroll
+    for (int j = 0; j < TJ; j++) fa[rb][j] = *(const bf16x8*)(sa + arow0 + 32 * j * 128 + ((c ^ fak[j]) << 4));
+  };
+
+  issue(0, 0);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (nk > 1) issue(1, 1);
+  frags(0, 0, 0);
+  for (int kt = 0; kt < nk; kt++) {
+    const int buf = kt & 1;
 #pragma unroll
     for (int s = 0; s < BK / 16; s++) {
-      const int slot = ((2 * s + half) ^ sw8) * 16;
-      bf16x8 fw[TI], fa[TJ];
-#pragma unroll
-      for (int i = 0; i < TI; i++) fw[i] = *(const bf16x8*)(sw + (wn * WTN + 32 * i + l32) * 128 + slot);
-#pragma unroll
-      for (int j = 0; j < TJ; j++) fa[j] = *(const bf16x8*)(sa + (wm * WTM + 32 * j + l32) * 128 + slot);
+      const int rb = s & 1;
+      if (s < BK / 16 - 1) {
+        frags(buf, s + 1, rb ^ 1);
+      } else if (kt + 1 < nk) {
+        __builtin_amdgcn_s_waitcnt(0);   // tile kt+1 landed and this wave's reads of `buf` are done
+        __syncthreads();                 // ... in every wave: `buf` may be refilled
+        if (kt + 2 < nk) issue(kt + 2, buf);
+        frags(buf ^ 1, 0, rb ^ 1);
+      }
 #pragma unroll
       for (int i = 0; i < TI; i++)
 #pragma unroll
-        for (int j = 0; j < TJ; j++) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[i], fa[j], acc[i][j], 0, 0, 0);
+        for (int j = 0; j < TJ; j++)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[rb][i], fa[rb][j], acc[i][j], 0, 0, 0);
+      // interleave one fragment read between consecutive MFMAs
+#pragma unroll
+      for (int q = 0; q < TI + TJ; q++) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+      if (TI * TJ > TI + TJ) __builtin_amdgcn_sched_group_barrier(0x008, TI * TJ - TI - TJ, 0);
     }
   }
 
   // accumulator (i, j), register r: n = 32i + 8(r/4) + 4*half + r%4, m = 32j + lane%32
 #pragma unroll
-  for (int i = 0; i < TI; i++) {
+  for (int j = 0; j < TJ; j++) {
+    int m = m0 + wm * WTM + 32 * j + l32;
+    if (m >= P.M) continue;
+    const RowEpi R = row_epi(P, m);
 #pragma unroll
-    for (int j = 0; j < TJ; j++) {
-      int m = m0 + wm * WTM + 32 * j + l32;
-      if (m >= P.M) continue;
+    for (int i = 0; i < TI; i++) {
 #pragma unroll
       for (int g = 0; g < 4; g++) {
         int n = n0 + wn * WTN + 32 * i + 8 * g + 4 * half;
         if (n < P.N) {
           float v[4] = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
-          if (OUTF32) epilogue4<EPI, u16, float>(P, m, n, v);
-          else epilogue4<EPI, u16, u16>(P, m, n, v);
+          if (OUTF32) epilogue4<EPI, u16, float>(P, R, n, v);
+          else epilogue4<EPI, u16, u16>(P, R, n, v);
         }
       }
     }
@@ -241,7 +299,7 @@ static hipError_t launch_bf16(const GemmPair& pr, hipStream_t s) {
     attr_set[dev] = true;
   }
   int grid = 8 * cdiv(total, 8);
-  gemm_bf16_kernel<BM, BN, WM, WN, EPI, OUTF32><<<grid, 256, lds, s>>>(pr, tiles[0], total);
+  gemm_bf16_kernel<BM, BN, WM, WN, EPI, OUTF32><<<grid, WM * WN * 64, lds, s>>>(pr, tiles[0], total);
   return hipGetLastError();
 }
 
@@ -255,7 +313,7 @@ static hipError_t dispatch_bf16(const GemmPair& pr, hipStream_t s) {
   }
   if (maxn <= 64) return launch_bf16<64, 64, 2, 2, EPI, OUTF32>(pr, s);
   if (big_tiles < 512) return launch_bf16<128, 128, 2, 2, EPI, OUTF32>(pr, s);
-  return launch_bf16<256, 256, 2, 2, EPI, OUTF32>(pr, s);
+  return launch_bf16<256, 256, 4, 2, EPI, OUTF32>(pr, s);
 }
 
 // ---------------------------------------------------------------------------
@@ -307,7 +365,7 @@ __global__ void __launch_bounds__(256) gemm_f32_kernel(GemmPair pr, int tiles0, 
 #pragma unroll
   for (int i = 0; i < 4; i++) {
     int m = m0 + tr * 4 + i, n = n0 + tc * 4;
-    if (m < P.M && n < P.N) epilogue4<EPI, float, float>(P, m, n, acc[i]);
+    if (m < P.M && n < P.N) epilogue4<EPI, float, float>(P, row_epi(P, m), n, acc[i]);
   }
 }
 
