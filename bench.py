@@ -41,7 +41,7 @@ def parse():
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--config", default="step_512_k16", choices=[k for k, v in si.CONFIGS.items() if v.blocks >= 1])
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-sample-seeds", type=int, default=1)
+    p.add_argument("--cpu-sample-seeds", type=int, default=16)
     return p.parse_args()
 
 

@@ -469,7 +469,10 @@ dit_status dit_block_forward(const dit_block_config* c, const dit_block_weights*
     qkv.p[i].hidden = D;
     qkv.p[i].grid_w = c->grid_w;
   }
-  if (c->rope) qkv.p[0].rope_tab = rope;
+  if (c->rope) {
+    qkv.p[0].rope_tab = rope;
+    qkv.p[0].rope_npos = std::max(c->grid_h, c->grid_w);
+  }
   TIMED("gemm_qkv_rope", gemm_flops(qkv), 0, s, gemm(qkv, EPI_QKV, c->dtype, false, s));
   // joint attention over [text ; image]; output o reuses the h buffer
   AttnArgs at{};
@@ -531,6 +534,9 @@ dit_status joint_attention(const void* q, const void* k, const void* v, void* o,
     if (st < 0 || (st * (int64_t)es) % 16) return fail(DIT_ERR_INVALID_ARG, "strides must be >= 0 and keep 16-byte rows");
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o))
     return fail(DIT_ERR_INVALID_ARG, "q/k/v/o must be 16-byte aligned");
+  // the bf16 kernel addresses the keys of one (sample, head) with 31-bit byte offsets
+  if (dtype == DIT_BF16 && (double)seq * qkv_stride_s * 2.0 >= 2147483648.0)
+    return fail(DIT_ERR_UNSUPPORTED, "seq * qkv_stride_s spans more than 2 GiB");
   AttnArgs a{};
   a.q = q;
   a.k = k;

@@ -59,7 +59,7 @@ struct GemmProblem {
   const float* gate; int64_t gate_bstride;
   // EPI_QKV: 2D RoPE on columns [0, 2*hidden) (q and k) of image rows
   const float* rope_tab;         // [npos][head_dim/4] pairs (cos, sin), null = no RoPE
-  int grid_w, head_dim, hidden;
+  int grid_w, head_dim, hidden, rope_npos;
 };
 
 struct GemmPair {              // up to two problems (image stream, text stream) in one launch

@@ -31,7 +31,7 @@ namespace dit {
 __device__ __forceinline__ float gelu_tanh_f(float z) {
   // 0.5 z (1 + tanh(u)) = z * sigmoid(2u), u = sqrt(2/pi) (z + 0.044715 z^3)
   float u2 = 2.0f * 0.7978845608028654f * fmaf(0.044715f * z, z * z, z);
-  return z / (1.0f + __builtin_amdgcn_exp2f(-u2 * 1.4426950408889634f));
+  return z * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-u2 * 1.4426950408889634f));
 }
 
 template <typename T> __device__ __forceinline__ void load4(const T* p, float* f);
@@ -259,22 +259,85 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_bf16_kernel(GemmPair pr, in
     }
   }
 
+  // ---- epilogue: bias, gate vectors and the RoPE table are staged in LDS once per tile ----
+  constexpr int LDS_BYTES = 2 * (A_BYTES + W_BYTES);
+  __syncthreads();   // every wave is done with the operand tiles
+  float* s_bias = (float*)smem;                       // [BN]
+  float* s_gate = s_bias + BN;                        // [nbt][BN]
+  const int rpb = (int)P.cmap.rows_per_batch;
+  const int bfirst = m0 / rpb;
+  const int nbt = (min(m0 + BM, P.M) - 1) / rpb - bfirst + 1;
+  const bool gate_lds = EPI == EPI_RESID && (size_t)(BN + nbt * BN) * 4 <= (size_t)LDS_BYTES;
+  float* s_rope = s_bias + BN;                        // [npos][head_dim/4][2] (QKV only)
+  const int rope_n = (EPI == EPI_QKV && P.rope_tab) ? P.rope_npos * (P.head_dim >> 1) : 0;
+  const bool rope_lds = rope_n > 0 && (size_t)(BN + rope_n) * 4 <= (size_t)LDS_BYTES;
+  for (int q = tid; q < BN; q += NW * 64)
+    s_bias[q] = (P.bias && n0 + q < P.N) ? to_f32(((const u16*)P.bias)[n0 + q]) : 0.f;
+  if (gate_lds)
+    for (int q = tid; q < nbt * BN; q += NW * 64) {
+      int bb = q / BN, nn = q - bb * BN;
+      s_gate[q] = n0 + nn < P.N ? P.gate[(int64_t)(bfirst + bb) * P.gate_bstride + n0 + nn] : 0.f;
+    }
+  if (rope_lds)
+    for (int q = tid; q < rope_n; q += NW * 64) s_rope[q] = P.rope_tab[q];
+  __syncthreads();
+
   // accumulator (i, j), register r: n = 32i + 8(r/4) + 4*half + r%4, m = 32j + lane%32
 #pragma unroll
   for (int j = 0; j < TJ; j++) {
     int m = m0 + wm * WTM + 32 * j + l32;
     if (m >= P.M) continue;
     const RowEpi R = row_epi(P, m);
-#pragma unroll
-    for (int i = 0; i < TI; i++) {
+    const int bt = m / rpb - bfirst;
+    // residual rows: prefetch the 32-column block i+1 while block i is finished
+    uint2 xr[2][4];
+    auto load_x = [&](int i, int slot) {
 #pragma unroll
       for (int g = 0; g < 4; g++) {
         int n = n0 + wn * WTN + 32 * i + 8 * g + 4 * half;
-        if (n < P.N) {
-          float v[4] = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
-          if (OUTF32) epilogue4<EPI, u16, float>(P, R, n, v);
-          else epilogue4<EPI, u16, u16>(P, R, n, v);
+        if (EPI == EPI_RESID && n < P.N) xr[slot][g] = *(const uint2*)((const u16*)P.C + R.off + n);
+      }
+    };
+    if (EPI == EPI_RESID) load_x(0, 0);
+#pragma unroll
+    for (int i = 0; i < TI; i++) {
+      if (EPI == EPI_RESID && i + 1 < TI) load_x(i + 1, (i + 1) & 1);
+#pragma unroll
+      for (int g = 0; g < 4; g++) {
+        int nl = wn * WTN + 32 * i + 8 * g + 4 * half;   // column inside the tile
+        int n = n0 + nl;
+        if (n >= P.N) continue;
+        float v[4] = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
+        float4 bv = *(const float4*)(s_bias + nl);
+        v[0] += bv.x; v[1] += bv.y; v[2] += bv.z; v[3] += bv.w;
+        if (EPI == EPI_GELU) {
+#pragma unroll
+          for (int q = 0; q < 4; q++) v[q] = gelu_tanh_f(v[q]);
         }
+        if (EPI == EPI_RESID) {
+          float4 gv = gate_lds ? *(const float4*)(s_gate + bt * BN + nl)
+                               : *(const float4*)(P.gate + R.gate + n);
+          uint2 u = xr[i & 1][g];
+          v[0] = fmaf(gv.x, v[0], __uint_as_float(u.x << 16));
+          v[1] = fmaf(gv.y, v[1], __uint_as_float(u.x & 0xffff0000u));
+          v[2] = fmaf(gv.z, v[2], __uint_as_float(u.y << 16));
+          v[3] = fmaf(gv.w, v[3], __uint_as_float(u.y & 0xffff0000u));
+        }
+        if (EPI == EPI_QKV && P.rope_tab && n < 2 * P.hidden) {
+          int dd = n & (P.head_dim - 1);
+          int hh = P.head_dim >> 1;
+          int pos = dd < hh ? R.rpos : R.cpos;
+          int pr = (dd & (hh - 1)) >> 1;
+          int ti = (pos * (P.head_dim >> 2) + pr) * 2;
+          float4 t = rope_lds ? *(const float4*)(s_rope + ti) : *(const float4*)(P.rope_tab + ti);
+          float a0 = v[0], b0 = v[1], a1 = v[2], b1 = v[3];
+          v[0] = a0 * t.x - b0 * t.y;
+          v[1] = a0 * t.y + b0 * t.x;
+          v[2] = a1 * t.z - b1 * t.w;
+          v[3] = a1 * t.w + b1 * t.z;
+        }
+        if (OUTF32) store4<float>((float*)P.C + R.off + n, v);
+        else store4<u16>((u16*)P.C + R.off + n, v);
       }
     }
   }
