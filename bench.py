@@ -42,7 +42,37 @@ def parse():
     p.add_argument("--config", default="step_512_k16", choices=[k for k, v in si.CONFIGS.items() if v.blocks >= 1])
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-sample-seeds", type=int, default=16)
+    p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                   help="only run 5 plain device copies of MIB MiB (torch copy kernel); used to scale the "
+                        "FETCH_SIZE / WRITE_SIZE counters to bytes")
     return p.parse_args()
+
+
+def copy_calibration(torch, mib):
+    n = mib * (1 << 20) // 4
+    src = torch.randn(n, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes_per_launch": n * 4, "launches": 5}), flush=True)
+
+
+def traffic_from_profile():
+    """HBM bytes per launch of the dominant kernel from the committed counter summary,
+    if it was taken on the current GEMM source (else None)."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "gemm_mlp_up_gelu_step_512_k16_traffic.json")
+    src = os.path.join(ROOT, "paper_2606_19004_amd", "csrc", "k_gemm.hip")
+    try:
+        rec = json.load(open(path))
+        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    except (OSError, ValueError):
+        return None
+    if rec.get("k_gemm_sha") != sha:
+        return None
+    return rec.get("hbm_bytes_per_launch")
 
 
 class DeviceInputs:
@@ -133,9 +163,12 @@ def main():
               "(no collectives); run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
     import torch
+    torch.cuda.set_device(0)
+    if args.copy_calibration:
+        copy_calibration(torch, args.copy_calibration)
+        return
     from paper_2606_19004_amd import ditstep as d
     cfg = si.CONFIGS[args.config]
-    torch.cuda.set_device(0)
     x = DeviceInputs(torch, d, cfg)
     step = make_step(d, cfg, x)
     for _ in range(args.warmup):
@@ -169,7 +202,8 @@ def main():
     per_launch = dom["flops"] / dom["launches"]
     achieved = per_launch / avg_s / 1e12
     roofline = {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None, "kernel": dom["name"],
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic_from_profile() if dom["name"] == "gemm_mlp_up_gelu" else None,
+                "kernel": dom["name"],
                 "flops_per_launch": per_launch, "avg_launch_us": round(avg_s * 1e6, 2)}
     gemm_ms = sum(k["total_ms"] for k in stats if k["name"].startswith("gemm"))
     gemm_fl = sum(k["flops"] for k in stats if k["name"].startswith("gemm"))

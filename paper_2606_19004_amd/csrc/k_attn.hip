@@ -13,7 +13,11 @@
 //     order the score accumulator already has, and operand A (V^T) is read in
 //     that same key order from a transposed V tile in LDS (two ds_read_b64).
 //   * K rows in LDS are 16-byte chunks XOR-swizzled by key, V^T rows padded by
-//     4 elements, so fragment reads are free of bank conflicts.
+//     4 elements, so fragment reads are free of bank conflicts; the fragments of
+//     the next MFMA step are read while the current step's MFMAs run.
+//   * Workgroups are dispatched round-robin over the 8 XCDs; each XCD gets a
+//     contiguous range of (sample, head, query block) tiles, so the query blocks
+//     of one (sample, head) read its K/V through the same L2.
 // fp32 path: one thread per query, K/V tiles in LDS (small configurations).
 #include "internal.h"
 
@@ -29,7 +33,15 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_bf16(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) u16 sK[2][KB * D];
   __shared__ __attribute__((aligned(16))) u16 sVt[2][D * VT];
 
-  const int b = blockIdx.z, h = blockIdx.y;
+  // XCD-aware order: workgroup ids go round-robin over the 8 XCDs; give each XCD a
+  // contiguous range of (sample, head, query-block) tiles so the query blocks of one
+  // (sample, head) share K/V through that XCD's L2.
+  const int nqb = cdiv(a.S, QB), per = (nqb * a.H * a.B + 7) / 8;
+  const int wid = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
+  const int lt = (wid & 7) * per + (wid >> 3);
+  if (lt >= nqb * a.H * a.B) return;
+  const int qblk = lt % nqb, bh = lt / nqb;
+  const int b = bh / a.H, h = bh % a.H;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int half = lane >> 5, l32 = lane & 31;
   const int S = a.S;
@@ -38,7 +50,7 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_bf16(AttnArgs a) {
   const u16* Vg = (const u16*)a.v + (int64_t)b * a.qs_b + (int64_t)h * a.qs_h;
 
   // this lane's query and its Q fragments: q[qi][16 s + 8 half + 0..7]
-  const int qi = blockIdx.x * QB + wave * 32 + l32;
+  const int qi = qblk * QB + wave * 32 + l32;
   bf16x8 qf[NKS];
   {
     const u16* qrow = Q + (int64_t)min(qi, S - 1) * a.qs_s;
@@ -96,19 +108,32 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_bf16(AttnArgs a) {
     const int buf = kt & 1;
     if (kt + 1 < nt) gload(kt + 1);   // next tile in flight during this tile's math
 
-    // S^T blocks: keys 32 kb + 8(r/4) + 4 half + r%4 of this lane's query
+    // S^T blocks: keys 32 kb + 8(r/4) + 4 half + r%4 of this lane's query.
+    // The KB/32 accumulator chains advance together; the K fragments of dim step
+    // s+1 are read while the MFMAs of step s run.
     f32x16 st[KB / 32];
 #pragma unroll
-    for (int kb = 0; kb < KB / 32; kb++) {
+    for (int kb = 0; kb < KB / 32; kb++)
 #pragma unroll
       for (int r = 0; r < 16; r++) st[kb][r] = 0.f;
-      const int key = 32 * kb + l32;
+    bf16x8 kf[2][KB / 32];
 #pragma unroll
-      for (int s = 0; s < NKS; s++) {
-        int slot = (2 * s + half) ^ (key % CH);
-        bf16x8 kf = *(const bf16x8*)(&sK[buf][key * D + slot * 8]);
-        st[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], st[kb], 0, 0, 0);
+    for (int kb = 0; kb < KB / 32; kb++) {
+      const int key = 32 * kb + l32;
+      kf[0][kb] = *(const bf16x8*)(&sK[buf][key * D + ((0 + half) ^ (key % CH)) * 8]);
+    }
+#pragma unroll
+    for (int s = 0; s < NKS; s++) {
+      if (s + 1 < NKS) {
+#pragma unroll
+        for (int kb = 0; kb < KB / 32; kb++) {
+          const int key = 32 * kb + l32;
+          kf[(s + 1) & 1][kb] = *(const bf16x8*)(&sK[buf][key * D + ((2 * (s + 1) + half) ^ (key % CH)) * 8]);
+        }
       }
+#pragma unroll
+      for (int kb = 0; kb < KB / 32; kb++)
+        st[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s & 1][kb], qf[s], st[kb], 0, 0, 0);
     }
     // mask keys past the end (last tile only)
     if ((kt + 1) * KB > S) {
@@ -147,20 +172,27 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_bf16(AttnArgs a) {
 #pragma unroll
       for (int r = 0; r < 16; r++) o[i][r] *= alpha;
 
-    // O^T[dim][query] += V^T[dim][keys] P^T[keys][query]
+    // O^T[dim][query] += V^T[dim][keys] P^T[keys][query]; the NDB output chains advance
+    // together over the KB/16 key steps, V^T fragments of step q+1 read during step q
+    bf16x8 vfr[2][NDB];
+    auto read_v = [&](int q, int slot) {
+      const int kb = q >> 1, t = q & 1;
 #pragma unroll
-    for (int db = 0; db < NDB; db++) {
-      const u16* vrow = &sVt[buf][(32 * db + l32) * VT];
+      for (int db = 0; db < NDB; db++) {
+        const u16* vrow = &sVt[buf][(32 * db + l32) * VT];
+        int k0 = 32 * kb + 16 * t + 4 * half;
+        bf16x4 lo = *(const bf16x4*)(vrow + k0);
+        bf16x4 hi = *(const bf16x4*)(vrow + k0 + 8);
+        vfr[slot][db] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+      }
+    };
+    read_v(0, 0);
 #pragma unroll
-      for (int kb = 0; kb < KB / 32; kb++)
+    for (int q = 0; q < KB / 16; q++) {
+      if (q + 1 < KB / 16) read_v(q + 1, (q + 1) & 1);
 #pragma unroll
-        for (int t = 0; t < 2; t++) {
-          int k0 = 32 * kb + 16 * t + 4 * half;
-          bf16x4 lo = *(const bf16x4*)(vrow + k0);
-          bf16x4 hi = *(const bf16x4*)(vrow + k0 + 8);
-          bf16x8 vf = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[kb][t], o[db], 0, 0, 0);
-        }
+      for (int db = 0; db < NDB; db++)
+        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vfr[q & 1][db], pf[q >> 1][q & 1], o[db], 0, 0, 0);
     }
     if (kt + 1 < nt) {
       sstore(buf ^ 1);   // buffer buf^1 was last read in iteration kt-1, before the barrier below it
@@ -241,7 +273,12 @@ __global__ void __launch_bounds__(64) attn_fwd_f32(AttnArgs a) {
 hipError_t attention(const AttnArgs& a, int dtype, hipStream_t s) {
   if (a.B == 0 || a.H == 0 || a.S == 0) return hipSuccess;
   if (dtype == DT_BF16) {
-    dim3 grid(cdiv(a.S, 128), a.H, a.B);
+    int nqb = cdiv(a.S, 128);
+    int total = nqb * a.H * a.B, per = cdiv(total, 8);
+    dim3 grid(nqb, a.H, a.B);
+    // the kernel maps linear id -> tile with ceil(total/8) tiles per XCD and ids past the
+    // tile count exit; a grid of exactly `total` ids covers every tile when total % 8 == 0
+    if (total % 8) grid = dim3(8 * per, 1, 1);
     if (a.d == 128) attn_fwd_bf16<128><<<grid, 256, 0, s>>>(a);
     else attn_fwd_bf16<64><<<grid, 256, 0, s>>>(a);
   } else {

@@ -306,6 +306,7 @@ __global__ void __launch_bounds__(256) gemv_kernel(GemvArgs a, int b0, int nb) {
 // [2][16][K]; each wave then streams 32 weight rows once and multiplies them
 // against both parts with v_mfma_f32_16x16x32_bf16 (samples are the MFMA's
 // 16-wide N dimension), so HBM bandwidth, not VALU FMAs, sets the time.
+// A workgroup owns 32 weight rows and splits K over its 4 waves.
 // ---------------------------------------------------------------------------
 __global__ void split_hilo_kernel(const float* __restrict__ in, int64_t stride, int b0, int nb, int K, int silu,
                                   u16* __restrict__ out) {
@@ -323,11 +324,13 @@ __global__ void split_hilo_kernel(const float* __restrict__ in, int64_t stride, 
 }
 
 __global__ void __launch_bounds__(256) gemv_mfma_kernel(GemvArgs a, const u16* __restrict__ xs, int b0, int nb) {
+  // one workgroup = 32 weight rows; its 4 waves take every 4th 32-deep k step and the
+  // partial sums meet in LDS, so each row block streams with 4 independent load chains
+  __shared__ f32x4 part[4][2][64];
   const int s = blockIdx.y;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int n0 = blockIdx.x * 128 + wave * 32;
-  if (n0 >= a.N) return;
-  const int K = a.K;
+  const int n0 = blockIdx.x * 32;
+  const int K = a.K, nks = K / 32;
   const int r16 = lane & 15, kq = (lane >> 4) * 8;
   // operand A: rows n0 + r16 and n0 + 16 + r16 (clamped; results of clamped rows are dropped)
   const u16* W = (const u16*)a.W[s];
@@ -337,15 +340,16 @@ __global__ void __launch_bounds__(256) gemv_mfma_kernel(GemvArgs a, const u16* _
   const u16* xh = xs + (int64_t)r16 * K + kq;
   const u16* xl = xs + (int64_t)(16 + r16) * K + kq;
   f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
-  int k = 0;
-  for (; k + 128 <= K; k += 128) {
+  int ks = wave;
+  for (; ks + 12 < nks; ks += 16) {
     bf16x8 fa[4], fb[4], fh[4], fl[4];
 #pragma unroll
     for (int u = 0; u < 4; u++) {
-      fa[u] = *(const bf16x8*)(w0 + k + 32 * u);
-      fb[u] = *(const bf16x8*)(w1 + k + 32 * u);
-      fh[u] = *(const bf16x8*)(xh + k + 32 * u);
-      fl[u] = *(const bf16x8*)(xl + k + 32 * u);
+      int k = 32 * (ks + 4 * u);
+      fa[u] = *(const bf16x8*)(w0 + k);
+      fb[u] = *(const bf16x8*)(w1 + k);
+      fh[u] = *(const bf16x8*)(xh + k);
+      fl[u] = *(const bf16x8*)(xl + k);
     }
 #pragma unroll
     for (int u = 0; u < 4; u++) {
@@ -355,13 +359,28 @@ __global__ void __launch_bounds__(256) gemv_mfma_kernel(GemvArgs a, const u16* _
       acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[u], fl[u], acc1, 0, 0, 0);
     }
   }
-  for (; k < K; k += 32) {
+  for (; ks < nks; ks += 4) {
+    int k = 32 * ks;
     bf16x8 fa = *(const bf16x8*)(w0 + k), fb = *(const bf16x8*)(w1 + k);
     bf16x8 fh = *(const bf16x8*)(xh + k), fl = *(const bf16x8*)(xl + k);
     acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa, fh, acc0, 0, 0, 0);
     acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa, fl, acc0, 0, 0, 0);
     acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb, fh, acc1, 0, 0, 0);
     acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb, fl, acc1, 0, 0, 0);
+  }
+  part[wave][0][lane] = acc0;
+  part[wave][1][lane] = acc1;
+  __syncthreads();
+  if (wave != 0) return;
+  // sum the 4 partials in a fixed order (deterministic)
+#pragma unroll
+  for (int w = 1; w < 4; w++) {
+    f32x4 p0 = part[w][0][lane], p1 = part[w][1][lane];
+#pragma unroll
+    for (int r = 0; r < 4; r++) {
+      acc0[r] += p0[r];
+      acc1[r] += p1[r];
+    }
   }
   // accumulator register r of lane l: weight row 4 (l / 16) + r, sample l % 16
   const int b = lane & 15;
@@ -381,7 +400,7 @@ hipError_t gemv_bf16(const GemvArgs& a, u16* xs, int silu_in, hipStream_t s) {
   for (int b0 = 0; b0 < a.B; b0 += 16) {
     int nb = std::min(16, a.B - b0);
     split_hilo_kernel<<<dim3(cdiv(a.K, 256), 16), 256, 0, s>>>(a.in, a.in_bstride, b0, nb, a.K, silu_in, xs);
-    gemv_mfma_kernel<<<dim3(cdiv(a.N, 128), a.nstreams), 256, 0, s>>>(a, xs, b0, nb);
+    gemv_mfma_kernel<<<dim3(cdiv(a.N, 32), a.nstreams), 256, 0, s>>>(a, xs, b0, nb);
   }
   return hipGetLastError();
 }
