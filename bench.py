@@ -32,6 +32,11 @@ import seeded_inputs as si  # noqa: E402
 
 PEAK_BF16_TFLOPS = 2516.6      # MI355X dense bf16 MFMA (256 CUs x 2.4 GHz x 4096 flop/clk)
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+TRAFFIC_JSON = "profiles/gemm_step_512_k16_traffic.json"
+KERNEL_MD = "profiles/step_512_k16_kernel_stats.md"
+# source file whose kernels each counted class runs (a summary is stale once that file changes)
+CLASS_SOURCE = {"gemm_qkv_rope": "k_gemm.hip", "gemm_out_gate": "k_gemm.hip", "gemm_mlp_up_gelu": "k_gemm.hip",
+                "gemm_mlp_down_gate": "k_gemm.hip", "attention": "k_attn.hip", "ln_modulate": "k_elementwise.hip"}
 
 
 def parse():
@@ -45,6 +50,12 @@ def parse():
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                    help="only run 5 plain device copies of MIB MiB (torch copy kernel); used to scale the "
                         "FETCH_SIZE / WRITE_SIZE counters to bytes")
+    p.add_argument("--traffic-summary", metavar="DIR", default=None,
+                   help="no GPU: turn the four rocprofv3 --pmc runs under DIR (calib_FETCH_SIZE, "
+                        "calib_WRITE_SIZE, bench_FETCH_SIZE, bench_WRITE_SIZE) into " + TRAFFIC_JSON)
+    p.add_argument("--kernel-summary", metavar="DIR", default=None,
+                   help="no GPU: turn rocprofv3 --kernel-trace --stats output under DIR (bench_kernel_stats.csv, "
+                        "bench_kernel_trace.csv) plus the bench JSON line in DIR/../bench.json into " + KERNEL_MD)
     return p.parse_args()
 
 
@@ -59,20 +70,157 @@ def copy_calibration(torch, mib):
     print(json.dumps({"copy_calibration_bytes_per_launch": n * 4, "launches": 5}), flush=True)
 
 
-def traffic_from_profile():
-    """HBM bytes per launch of the dominant kernel from the committed counter summary,
-    if it was taken on the current GEMM source (else None)."""
+def source_sha(name):
     import hashlib
-    path = os.path.join(ROOT, "profiles", "gemm_mlp_up_gelu_step_512_k16_traffic.json")
-    src = os.path.join(ROOT, "paper_2606_19004_amd", "csrc", "k_gemm.hip")
+    with open(os.path.join(ROOT, "paper_2606_19004_amd", "csrc", name), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def traffic_from_profile(kernel_class):
+    """Measured HBM bytes per launch of one kernel class from the committed counter summary, or
+    None when there is none or it was taken on another version of that kernel's source."""
     try:
-        rec = json.load(open(path))
-        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
-    except (OSError, ValueError):
+        rec = json.load(open(os.path.join(ROOT, TRAFFIC_JSON)))
+        c = rec["per_kernel_class"][kernel_class]
+        if c["source_sha"] != source_sha(CLASS_SOURCE[kernel_class]):
+            return None
+        return c["hbm_bytes_per_launch"]
+    except (OSError, ValueError, KeyError):
         return None
-    if rec.get("k_gemm_sha") != sha:
-        return None
-    return rec.get("hbm_bytes_per_launch")
+
+
+def classify_dispatches(rows):
+    """Kernel class of every dispatch of one denoise-step run, in dispatch order. The two gated
+    residual GEMMs of a block share one kernel; the out-projection always precedes the MLP down."""
+    import re
+    resid_seen = 0
+    out = []
+    for r in rows:
+        n = r["Kernel_Name"]
+        m = re.search(r"gemm_bf16_kernel<(\d+), (\d+), (\d+), (\d+), (\d+)", n)
+        cls = None
+        if m and int(m.group(1)) == 256:
+            epi = int(m.group(5))
+            if epi == 3:
+                cls = "gemm_qkv_rope"
+            elif epi == 1:
+                cls = "gemm_mlp_up_gelu"
+            elif epi == 2:
+                cls = "gemm_out_gate" if resid_seen % 2 == 0 else "gemm_mlp_down_gate"
+                resid_seen += 1
+        elif "attn_fwd" in n:
+            cls = "attention"
+        elif "ln_modulate_kernel" in n:
+            cls = "ln_modulate"
+        out.append(cls)
+    return out
+
+
+def kernel_summary(run_dir, bench_json):
+    """Writes the kernel-time summary: rocprofv3's per-kernel stats, per-class averages from the
+    per-dispatch trace, and bench.py's own event timing of the same classes for comparison."""
+    import csv
+    with open(os.path.join(run_dir, "bench_kernel_stats.csv")) as f:
+        stats = [r for r in csv.DictReader(f) if "dit::" in r["Name"]]
+    with open(os.path.join(run_dir, "bench_kernel_trace.csv")) as f:
+        trace = sorted(csv.DictReader(f), key=lambda r: int(r["Start_Timestamp"]))
+    per = {}
+    for r, cls in zip(trace, classify_dispatches(trace)):
+        if cls:
+            per.setdefault(cls, []).append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-3)
+    with open(bench_json) as f:
+        b = json.loads([ln for ln in f if ln.startswith("{")][-1])
+    lines = ["# Kernel time summary: full K=16 denoise step (step_512_k16)", "",
+             "Workload: 8 dual-stream MMDiT blocks, hidden 3072, 24x128 heads, 1024 image + 256 text tokens, "
+             "K=16 seeds,", "SDE flow update, reward statistics 64x16 (bf16 weights and activations, fp32 "
+             "accumulation).", "", "Commands (repo root, on one MI355X):", "",
+             f"    rocprofv3 --kernel-trace --stats --output-format csv -d {run_dir} -o bench -- python3 bench.py "
+             "--steps 5 --warmup 2 --no-cpu-baseline",
+             f"    python3 bench.py --kernel-summary {run_dir}", "",
+             "The trace covers the bench's setup (torch kernels that draw the synthetic weights) plus 5 + 2 "
+             "timed/warm-up steps", "and one event-instrumented step (8 steps in all). Library kernels, sorted "
+             "by total time:", "", "| kernel | calls | avg us | total ms |", "|---|---|---|---|"]
+    for r in stats:
+        name = r["Name"].split("(")[0]
+        lines.append(f"| `{name}` | {r['Calls']} | {float(r['AverageNs']) * 1e-3:.2f} | "
+                     f"{float(r['TotalDurationNs']) * 1e-6:.3f} |")
+    lines += ["", "Per kernel class (classified per dispatch from the trace; `gemm_bf16_kernel<..., 2, ...>` runs "
+              "both the output projection and the MLP down, in that order within a block), against bench.py's "
+              "HIP-event average of the same class in a run without the profiler:", "",
+              "| class | dispatches | rocprofv3 avg us | bench.py events avg us |", "|---|---|---|---|"]
+    for cls, v in sorted(per.items(), key=lambda kv: -sum(kv[1])):
+        ev = b.get("kernels", {}).get(cls, {}).get("avg_us")
+        lines.append(f"| {cls} | {len(v)} | {sum(v) / len(v):.2f} | {ev if ev is not None else '-'} |")
+    r = b["roofline"]
+    lines += ["", f"bench.py (no profiler): {b['value']} ms per step; dominant kernel `{r['kernel']}` averaged "
+              f"{r['avg_launch_us']} us per launch with HIP events ({r['achieved']} TFLOP/s, "
+              f"{100 * r['frac']:.1f}% of {r['peak']}).",
+              "EPI codes in `gemm_bf16_kernel<BM, BN, WM, WN, EPI, OUTF32, MS>`: 0 plain store, 1 GELU (MLP up), "
+              "2 gated residual (output projection, MLP down), 3 QKV with 2D RoPE; MS is the MFMA block size."]
+    with open(os.path.join(ROOT, KERNEL_MD), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def traffic_summary(run_dir, cfg):
+    """Writes the per-class HBM traffic summary from four rocprofv3 --pmc runs: FETCH_SIZE and
+    WRITE_SIZE (KiB per dispatch) of a 1 GiB device copy, then of bench.py --steps 1 --warmup 1.
+    Each counter is scaled by bytes copied / counter read for the copy kernel."""
+    import csv
+    import glob
+
+    def rows(sub):
+        files = glob.glob(os.path.join(run_dir, sub, "*counter_collection.csv"))
+        if not files:
+            raise SystemExit(f"no counter_collection.csv under {os.path.join(run_dir, sub)}")
+        with open(files[0]) as f:
+            return [r for r in csv.DictReader(f)]
+
+    copy_bytes = 1024 * (1 << 20)
+    scale, calib = {}, {}
+    for c in ("FETCH_SIZE", "WRITE_SIZE"):
+        vals = [float(r["Counter_Value"]) for r in rows("calib_" + c) if "copyBuffer" in r["Kernel_Name"]]
+        kib = sorted(vals)[len(vals) // 2]
+        calib[c + "_kib_per_launch"] = kib
+        scale[c] = copy_bytes / (kib * 1024.0)
+    per = {}
+    for c in ("FETCH_SIZE", "WRITE_SIZE"):
+        rr = rows("bench_" + c)
+        for r, cls in zip(rr, classify_dispatches(rr)):
+            if cls:
+                per.setdefault(cls, {}).setdefault(c, []).append(float(r["Counter_Value"]))
+    M, D, F = cfg.batch * cfg.seq, cfg.hidden, cfg.mlp_hidden
+    algo = {"gemm_qkv_rope": 2 * (M * D + 3 * D * D + 3 * M * D),
+            "gemm_out_gate": 2 * (M * D + D * D + 2 * M * D),
+            "gemm_mlp_up_gelu": 2 * (M * D + F * D + M * F),
+            "gemm_mlp_down_gate": 2 * (M * F + D * F + 2 * M * D),
+            "attention": 2 * 4 * M * D,
+            "ln_modulate": 2 * 2 * M * D}
+    classes = {}
+    for cls, v in per.items():
+        fk = sum(v["FETCH_SIZE"]) / len(v["FETCH_SIZE"])
+        wk = sum(v["WRITE_SIZE"]) / len(v["WRITE_SIZE"])
+        fb, wb = fk * 1024 * scale["FETCH_SIZE"], wk * 1024 * scale["WRITE_SIZE"]
+        classes[cls] = {"launches_counted": len(v["FETCH_SIZE"]), "fetch_kib_per_launch": round(fk, 1),
+                        "write_kib_per_launch": round(wk, 1), "fetch_bytes_per_launch": round(fb),
+                        "write_bytes_per_launch": round(wb), "hbm_bytes_per_launch": round(fb + wb),
+                        "algorithmic_bytes_per_launch": algo[cls],
+                        "measured_over_algorithmic": round((fb + wb) / algo[cls], 3),
+                        "source": CLASS_SOURCE[cls], "source_sha": source_sha(CLASS_SOURCE[cls])}
+    rec = {"workload": f"{cfg.name} (M={M} rows of image+text tokens over K={cfg.batch} seeds, hidden {D}, "
+                       f"MLP {F})",
+           "calibration": dict(calib, kernel="__amd_rocclr_copyBuffer, 1 GiB device copy",
+                               bytes_per_launch=copy_bytes, fetch_scale=round(scale["FETCH_SIZE"], 5),
+                               write_scale=round(scale["WRITE_SIZE"], 5)),
+           "commands": [f"rocprofv3 --pmc {c} --output-format csv -d {run_dir}/{k}_{c} -o {k[0]} -- python3 bench.py "
+                        + ("--copy-calibration 1024" if k == "calib" else "--steps 1 --warmup 1 --no-cpu-baseline")
+                        for k in ("calib", "bench") for c in ("FETCH_SIZE", "WRITE_SIZE")]
+                       + [f"python3 bench.py --traffic-summary {run_dir}"],
+           "per_kernel_class": classes}
+    with open(os.path.join(ROOT, TRAFFIC_JSON), "w") as f:
+        json.dump(rec, f, indent=1)
+        f.write("\n")
+    print(json.dumps({k: v["measured_over_algorithmic"] for k, v in classes.items()}))
 
 
 class DeviceInputs:
@@ -157,6 +305,12 @@ def cpu_baseline(cfg, n_seeds):
 
 def main():
     args = parse()
+    if args.traffic_summary:
+        traffic_summary(args.traffic_summary, si.CONFIGS[args.config])
+        return
+    if args.kernel_summary:
+        kernel_summary(args.kernel_summary, os.path.join(args.kernel_summary, "..", "bench.json"))
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU: this build runs the denoise step on a single MI355X "
@@ -202,7 +356,7 @@ def main():
     per_launch = dom["flops"] / dom["launches"]
     achieved = per_launch / avg_s / 1e12
     roofline = {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic_from_profile() if dom["name"] == "gemm_mlp_up_gelu" else None,
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic_from_profile(dom["name"]),
                 "kernel": dom["name"],
                 "flops_per_launch": per_launch, "avg_launch_us": round(avg_s * 1e6, 2)}
     gemm_ms = sum(k["total_ms"] for k in stats if k["name"].startswith("gemm"))
