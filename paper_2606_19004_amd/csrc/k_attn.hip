@@ -3,6 +3,10 @@
 // bf16 path (head_dim 64 or 128): flash-style, one workgroup = 4 waves = 128
 // queries of one (sample, head); K/V tiles of 64 keys staged in LDS and shared
 // by the 4 waves; online softmax in the exp2 domain with fp32 statistics.
+//   * K and V tiles go from global memory straight into LDS (buffer loads with the
+//     LDS-destination bit), double-buffered: tile t+1 streams in while tile t is
+//     multiplied. The buffer resource spans exactly this (sample, head)'s rows, so
+//     keys past the end read as zeros with no bounds arithmetic.
 //   * Scores are computed transposed, S^T = K Q^T, with v_mfma_f32_32x32x16_bf16:
 //     operand A = 32 keys (K rows from LDS), operand B = 32 queries (Q rows held
 //     in registers for the whole loop). Each lane then owns ONE query column
@@ -10,11 +14,18 @@
 //     max and row sum need in-lane reductions plus one exchange with lane^32.
 //   * O^T = V^T P^T: P^T is consumed straight from the score registers (rounded
 //     to bf16) as operand B; the key order inside a 16-key MFMA step is the
-//     order the score accumulator already has, and operand A (V^T) is read in
-//     that same key order from a transposed V tile in LDS (two ds_read_b64).
-//   * K rows in LDS are 16-byte chunks XOR-swizzled by key, V^T rows padded by
-//     4 elements, so fragment reads are free of bank conflicts; the fragments of
-//     the next MFMA step are read while the current step's MFMAs run.
+//     order the score accumulator already has. Operand A (V^T) comes from the
+//     row-major V tile through ds_read_b64_tr_b16, the LDS read that transposes
+//     16-bit elements across each group of 16 lanes: lane s of a group points at
+//     4 consecutive dims of key k0 + s/4, and lane j of the group receives keys
+//     k0..k0+3 of dim j, which is exactly a quarter of an A fragment.
+//   * LDS rows are 16-byte chunks XOR-swizzled by row (K: by key mod chunks per
+//     row; V: by key mod 4 in steps of a quarter row), so both the K fragment
+//     reads and the transposing V reads are free of bank conflicts.
+//   * Lazy rescaling: the running max only moves (and the output is only rescaled)
+//     when a row's new max exceeds it by more than TAU in the exp2 domain, so
+//     probabilities stay below 2^TAU; the normalisation divides by a row sum taken
+//     against the same max, so the result is unchanged.
 //   * Workgroups are dispatched round-robin over the 8 XCDs; each XCD gets a
 //     contiguous range of (sample, head, query block) tiles, so the query blocks
 //     of one (sample, head) read its K/V through the same L2.
@@ -23,15 +34,24 @@
 
 namespace dit {
 
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x8 __attribute__((ext_vector_type(8)));
+
 template <int D>
 __global__ void __launch_bounds__(256, 2) attn_fwd_bf16(AttnArgs a) {
   constexpr int QB = 128, KB = 64;
-  constexpr int CH = D / 8;            // 16-byte chunks per K row
-  constexpr int VT = KB + 4;           // padded V^T row (keys)
+  constexpr int CH = D / 8;            // 16-byte chunks per K/V row
+  constexpr int RB = D * 2;            // bytes per K/V row
+  constexpr int TILE = KB * RB;        // bytes per K (or V) tile
   constexpr int NDB = D / 32;          // 32-dim output blocks
   constexpr int NKS = D / 16;          // 16-dim steps of QK^T
-  __shared__ __attribute__((aligned(16))) u16 sK[2][KB * D];
-  __shared__ __attribute__((aligned(16))) u16 sVt[2][D * VT];
+  constexpr int KPI = 64 / CH;         // rows per 1 KB wave load
+  constexpr int LOADS = KB / KPI / 4;  // wave loads per wave per tile, for K and for V each
+  constexpr float TAU = 8.f;           // lazy-rescale threshold (log2 units)
+  static_assert(LOADS >= 1, "tile too small for 4 waves");
+#if defined(__HIP_DEVICE_COMPILE__)  // the buffer-resource builtins exist only in the device pass
+  __shared__ __attribute__((aligned(1024))) char smem[4 * TILE];   // [K0][K1][V0][V1]
 
   // XCD-aware order: workgroup ids go round-robin over the 8 XCDs; give each XCD a
   // contiguous range of (sample, head, query-block) tiles so the query blocks of one
@@ -58,82 +78,82 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_bf16(AttnArgs a) {
     for (int s = 0; s < NKS; s++) qf[s] = *(const bf16x8*)(qrow + 16 * s + 8 * half);
   }
 
-  // tile loader: KB*CH chunks of K and of V, (KB*CH)/256 per thread each
-  constexpr int LPT = KB * CH / 256;
-  uint4 kreg[LPT], vreg[LPT];
-  auto gload = [&](int kt) {
+  // direct-to-LDS loads: wave load i of this wave fills rows R0..R0+KPI-1 of a tile
+  // (R0 = (wave * LOADS + i) * KPI); lane -> row R0 + lane / CH, LDS slot lane % CH,
+  // which holds global chunk slot ^ swizzle(row)
+  const uint32_t rowstride = (uint32_t)(a.qs_s * 2);
+  const uint32_t nrec = (uint32_t)((int64_t)(S - 1) * a.qs_s * 2 + RB);
+  __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc((void*)Kg, (short)0, (int)nrec, 0x00020000);
+  __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc((void*)Vg, (short)0, (int)nrec, 0x00020000);
+  uint32_t koff[LOADS], voff[LOADS];
 #pragma unroll
-    for (int i = 0; i < LPT; i++) {
-      int idx = tid + 256 * i;
-      int key = idx % KB, c = idx / KB;   // consecutive lanes -> consecutive keys
-      int gk = kt * KB + key;
-      if (gk < S) {
-        kreg[i] = *(const uint4*)(Kg + (int64_t)gk * a.qs_s + c * 8);
-        vreg[i] = *(const uint4*)(Vg + (int64_t)gk * a.qs_s + c * 8);
-      } else {
-        kreg[i] = make_uint4(0, 0, 0, 0);
-        vreg[i] = make_uint4(0, 0, 0, 0);
-      }
+  for (int i = 0; i < LOADS; i++) {
+    const int row = (wave * LOADS + i) * KPI + lane / CH, slot = lane % CH;
+    koff[i] = row * rowstride + ((slot ^ (row % CH)) << 4);
+    voff[i] = row * rowstride + ((slot ^ ((row & 3) * (CH / 4))) << 4);
+  }
+  auto issue = [&](int kt, int buf) {
+    const uint32_t base = (uint32_t)(kt * KB) * rowstride;
+#pragma unroll
+    for (int i = 0; i < LOADS; i++) {
+      const int dst = (wave * LOADS + i) * KPI * RB;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_ptr_t)(smem + buf * TILE + dst), 16, base + koff[i], 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_ptr_t)(smem + (2 + buf) * TILE + dst), 16, base + voff[i], 0, 0,
+                                               0);
     }
   };
-  auto sstore = [&](int buf) {
+
+  // K fragment of key row 32 kb + l32, dim chunk 2 s + half (swizzle key % CH = l32 % CH)
+  const int ksw = l32 % CH;
+  const int krow = l32 * RB;
+  // V^T fragment quarters: lane reads 4 dims (8 bytes) of key 4 half + (lane >> 2) % 4 (+ step
+  // offsets); dims 32 db + 16 ((lane >> 4) & 1) + 4 (lane & 3), i.e. chunk
+  // 4 db + 2 ((lane >> 4) & 1) + ((lane >> 1) & 1), byte 8 (lane & 1) inside it
+  const int vkey = 4 * half + ((lane >> 2) & 3);
+  const int vsw = ((lane >> 2) & 3) * (CH / 4);
+  int vbase[NDB];
 #pragma unroll
-    for (int i = 0; i < LPT; i++) {
-      int idx = tid + 256 * i;
-      int key = idx % KB, c = idx / KB;
-      int slot = c ^ (key % CH);
-      *(uint4*)(&sK[buf][key * D + slot * 8]) = kreg[i];
-      uint32_t w[4] = {vreg[i].x, vreg[i].y, vreg[i].z, vreg[i].w};
-#pragma unroll
-      for (int e = 0; e < 4; e++) {
-        sVt[buf][(c * 8 + 2 * e) * VT + key] = (u16)(w[e] & 0xffff);
-        sVt[buf][(c * 8 + 2 * e + 1) * VT + key] = (u16)(w[e] >> 16);
-      }
-    }
-  };
+  for (int db = 0; db < NDB; db++) {
+    const int ch = 4 * db + 2 * ((lane >> 4) & 1) + ((lane >> 1) & 1);
+    vbase[db] = vkey * RB + ((ch ^ vsw) << 4) + 8 * (lane & 1);
+  }
 
   f32x16 o[NDB];
 #pragma unroll
   for (int i = 0; i < NDB; i++)
 #pragma unroll
     for (int r = 0; r < 16; r++) o[i][r] = 0.f;
+  const f32x16 zero = {};
   const float c = a.scale * 1.4426950408889634f;  // fold log2(e) into the scale
   float m_run = -INFINITY, l_run = 0.f;
 
   const int nt = cdiv(S, KB);
-  gload(0);
-  sstore(0);
+  issue(0, 0);
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   for (int kt = 0; kt < nt; kt++) {
     const int buf = kt & 1;
-    if (kt + 1 < nt) gload(kt + 1);   // next tile in flight during this tile's math
+    if (kt + 1 < nt) issue(kt + 1, buf ^ 1);   // buf^1 was last read before the previous barrier
+    const char* sk = smem + buf * TILE;
+    const char* sv = smem + (2 + buf) * TILE;
 
-    // S^T blocks: keys 32 kb + 8(r/4) + 4 half + r%4 of this lane's query.
-    // The KB/32 accumulator chains advance together; the K fragments of dim step
-    // s+1 are read while the MFMAs of step s run.
+    // S^T blocks: keys 32 kb + 8(r/4) + 4 half + r%4 of this lane's query. The K fragments of
+    // dim step s+1 are read while the MFMAs of step s run.
     f32x16 st[KB / 32];
-#pragma unroll
-    for (int kb = 0; kb < KB / 32; kb++)
-#pragma unroll
-      for (int r = 0; r < 16; r++) st[kb][r] = 0.f;
     bf16x8 kf[2][KB / 32];
 #pragma unroll
-    for (int kb = 0; kb < KB / 32; kb++) {
-      const int key = 32 * kb + l32;
-      kf[0][kb] = *(const bf16x8*)(&sK[buf][key * D + ((0 + half) ^ (key % CH)) * 8]);
-    }
+    for (int kb = 0; kb < KB / 32; kb++)
+      kf[0][kb] = *(const bf16x8*)(sk + 32 * kb * RB + krow + ((half ^ ksw) << 4));
 #pragma unroll
     for (int s = 0; s < NKS; s++) {
       if (s + 1 < NKS) {
 #pragma unroll
-        for (int kb = 0; kb < KB / 32; kb++) {
-          const int key = 32 * kb + l32;
-          kf[(s + 1) & 1][kb] = *(const bf16x8*)(&sK[buf][key * D + ((2 * (s + 1) + half) ^ (key % CH)) * 8]);
-        }
+        for (int kb = 0; kb < KB / 32; kb++)
+          kf[(s + 1) & 1][kb] = *(const bf16x8*)(sk + 32 * kb * RB + krow + (((2 * (s + 1) + half) ^ ksw) << 4));
       }
 #pragma unroll
       for (int kb = 0; kb < KB / 32; kb++)
-        st[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s & 1][kb], qf[s], st[kb], 0, 0, 0);
+        st[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s & 1][kb], qf[s], s == 0 ? zero : st[kb], 0, 0, 0);
     }
     // mask keys past the end (last tile only)
     if ((kt + 1) * KB > S) {
@@ -151,9 +171,17 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_bf16(AttnArgs a) {
 #pragma unroll
       for (int r = 0; r < 16; r++) mx = fmaxf(mx, st[kb][r]);
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));   // the other 16 keys of each 32-key block
-    const float m_new = fmaxf(m_run, mx * c);
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-    m_run = m_new;
+    const float mxs = mx * c;
+    if (__ballot(mxs > m_run + TAU) != 0) {   // some row's max moved by more than TAU
+      const float m_new = fmaxf(m_run, mxs);
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int i = 0; i < NDB; i++)
+#pragma unroll
+        for (int r = 0; r < 16; r++) o[i][r] *= alpha;
+    }
     float psum = 0.f;
     bf16x8 pf[KB / 32][2];
 #pragma unroll
@@ -162,28 +190,24 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_bf16(AttnArgs a) {
       for (int t = 0; t < 2; t++)
 #pragma unroll
         for (int j = 0; j < 8; j++) {
-          float p = __builtin_amdgcn_exp2f(fmaf(st[kb][8 * t + j], c, -m_new));
+          float p = __builtin_amdgcn_exp2f(fmaf(st[kb][8 * t + j], c, -m_run));
           psum += p;
           pf[kb][t][j] = (__bf16)p;
         }
-    l_run = fmaf(l_run, alpha, psum);
-#pragma unroll
-    for (int i = 0; i < NDB; i++)
-#pragma unroll
-      for (int r = 0; r < 16; r++) o[i][r] *= alpha;
+    l_run += psum;
 
-    // O^T[dim][query] += V^T[dim][keys] P^T[keys][query]; the NDB output chains advance
-    // together over the KB/16 key steps, V^T fragments of step q+1 read during step q
+    // O^T[dim][query] += V^T[dim][keys] P^T[keys][query] over the KB/16 key steps; the V^T
+    // fragments of step q+1 are read during step q. Step q covers keys 16 q + {4 half + 0..3,
+    // 8 + 4 half + 0..3}, the order of the score accumulator.
     bf16x8 vfr[2][NDB];
     auto read_v = [&](int q, int slot) {
-      const int kb = q >> 1, t = q & 1;
 #pragma unroll
       for (int db = 0; db < NDB; db++) {
-        const u16* vrow = &sVt[buf][(32 * db + l32) * VT];
-        int k0 = 32 * kb + 16 * t + 4 * half;
-        bf16x4 lo = *(const bf16x4*)(vrow + k0);
-        bf16x4 hi = *(const bf16x4*)(vrow + k0 + 8);
-        vfr[slot][db] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        const char* p0 = sv + 16 * q * RB + vbase[db];
+        i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(p0));
+        i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(p0 + 8 * RB));
+        i16x8 w = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        vfr[slot][db] = __builtin_bit_cast(bf16x8, w);
       }
     };
     read_v(0, 0);
@@ -194,10 +218,8 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_bf16(AttnArgs a) {
       for (int db = 0; db < NDB; db++)
         o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vfr[q & 1][db], pf[q >> 1][q & 1], o[db], 0, 0, 0);
     }
-    if (kt + 1 < nt) {
-      sstore(buf ^ 1);   // buffer buf^1 was last read in iteration kt-1, before the barrier below it
-    }
-    __syncthreads();
+    __builtin_amdgcn_s_waitcnt(0);   // this wave's share of tile kt+1 landed; its reads of buf are done
+    __syncthreads();                 // ... in every wave
   }
 
   // normalise: full row sum = this lane's part + lane^32's part
@@ -216,6 +238,7 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_bf16(AttnArgs a) {
         *(uint2*)(orow + dim) = u;
       }
   }
+#endif
 }
 
 // ---------------------------------------------------------------------------

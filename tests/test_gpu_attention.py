@@ -87,3 +87,27 @@ def test_attention_full_size_sampled(d, name):
         x = si.as_f64(q[bi, :, :, hi], "bf16")        # [S][3][d]
         ref = O.attention(x[rows, 0], x[:, 1], x[:, 2])
         assert rel_err(got[bi, rows, hi], ref) <= TOL_BF16
+
+
+@pytest.mark.parametrize("step,hd", [(10.0, 128), (3.0, 128), (10.0, 64), (-6.0, 128)])
+def test_attention_running_max_moves_across_tiles(d, step, hd):
+    """Scores that grow (or shrink) steadily along the key sequence: the row max in the exp2
+    domain moves by `step` per 64-key tile, so the kernel's running max is raised on many tiles
+    (step > 8, the lazy-rescale threshold), only every few tiles with probabilities up to 2^8
+    in between (step 3), or never after the first tile (step < 0)."""
+    rng = np.random.default_rng(int(abs(step) * 10) + hd)
+    b, s, h = 2, 450, 2
+    e = np.ones(hd) / math.sqrt(hd)
+    ab = step * math.sqrt(hd) / math.log2(math.e)      # q.k/sqrt(d) in log2 units grows by `step` per tile
+    x = np.empty((b, s, 3, h, hd), np.float32)
+    x[:, :, 0] = 4.0 * e + 0.05 * rng.standard_normal((b, s, h, hd))
+    ramp = (np.arange(s) / 64.0)[None, :, None, None] * (ab / 4.0)
+    x[:, :, 1] = ramp * e + 0.05 * rng.standard_normal((b, s, h, hd))
+    x[:, :, 2] = rng.standard_normal((b, s, h, hd))
+    st = si.stored(x, "bf16")
+    got = _run(d, st, b, s, h, hd, "bf16")
+    xs = si.as_f64(st, "bf16")
+    assert np.all(np.isfinite(got))
+    for bi in range(b):
+        ref = O.joint_attention(xs[bi, :, 0], xs[bi, :, 1], xs[bi, :, 2])
+        assert rel_err(got[bi], ref) <= TOL_BF16
