@@ -283,6 +283,37 @@ def flow_step(x, v, eps, t, t_next, a):
     return x + h * (v - 0.5 * sigma * sigma * score) + sigma * math.sqrt(-h) * eps
 
 
+def flow_mean(x, v, t, t_next, a):
+    """Mean of the SDE step's transition: the step above without its noise term."""
+    h = t_next - t
+    sigma = sde_sigma(t, a)
+    score = -(x + (1.0 - t) * v) / t
+    return x + h * (v - 0.5 * sigma * sigma * score)
+
+
+def flow_logprob(x, v, x_next, t, t_next, a):
+    """Log-density of x_next under the SDE step's Gaussian transition from x, per sample.
+
+    The step draws x' = mean(x, v) + sigma sqrt(-h) eps with eps ~ N(0, I), so
+    x' ~ N(mean, sigma^2 (-h) I); this is the per-sample likelihood that FlowGRPO's
+    policy ratio is built from (section 5: FlowGRPO is the algorithm backbone).
+    Reduced by summation over all latent elements of a sample (rows of the
+    [batch][n] inputs): the exact log-density. The deterministic ODE step (a == 0)
+    has no density; h >= 0 is not a denoising step. Both raise ValueError."""
+    h = t_next - t
+    if not a > 0.0:
+        raise ValueError("flow_logprob needs noise_level a > 0 (the ODE step has no density)")
+    if not (0.0 < t < 1.0) or not h < 0.0:
+        raise ValueError("flow_logprob needs 0 < t < 1 and t_next < t")
+    x = np.atleast_2d(np.asarray(x, dtype=np.float64))
+    v = np.atleast_2d(np.asarray(v, dtype=np.float64))
+    xn = np.atleast_2d(np.asarray(x_next, dtype=np.float64))
+    var = sde_sigma(t, a) ** 2 * (-h)
+    r = xn - flow_mean(x, v, t, t_next, a)
+    n = x.shape[1]
+    return -(r * r).sum(axis=1) / (2.0 * var) - 0.5 * n * math.log(2.0 * math.pi * var)
+
+
 # ---------------------------------------------------------------------------
 # per prompt-group reward statistics and seed selection
 # ---------------------------------------------------------------------------
