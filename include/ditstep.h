@@ -177,6 +177,21 @@ dit_status joint_attention(const void* q, const void* k, const void* v, void* o,
 dit_status flow_step(float* x, const float* v, const float* noise, int64_t n,
                      float t, float t_next, float noise_level, dit_stream stream);
 
+/* Log-density of x_next under the SDE step's Gaussian transition from x (the per-sample
+ * likelihood behind FlowGRPO's policy ratio; FlowGRPO is the paper's algorithm backbone,
+ * section 5). With h = t_next - t and sigma = a sqrt(t/(1-t)) as in flow_step,
+ *   mean = x + h (v + sigma^2/(2t) (x + (1-t) v)),  var = sigma^2 (-h),
+ *   logp[b] = -sum_i (x_next - mean)^2 / (2 var) - n/2 log(2 pi var)
+ * summed over the n_per_sample elements of sample b (rows of [batch][n_per_sample]
+ * fp32 device arrays x, v, x_next). Output logp [batch] fp64 on the device; the sum is
+ * taken in fp64 in a fixed order (one workgroup per sample), so it is deterministic.
+ * Errors: DIT_ERR_DOMAIN unless noise_level > 0, 0 < t < 1 and t_next < t (the ODE step
+ * has no density); DIT_ERR_INVALID_ARG for NULL pointers or negative sizes. batch == 0 or
+ * n_per_sample == 0 writes zeros (n == 0) or nothing (batch == 0). */
+dit_status flow_logprob(const float* x, const float* v, const float* x_next, int32_t batch,
+                        int64_t n_per_sample, float t, float t_next, float noise_level, double* logp,
+                        dit_stream stream);
+
 /* Per prompt-group statistics over rewards [G][n] fp32 (row g = the n seeds
  * of prompt group g):
  *   mean[g] = sum_j r / n; std[g] = sqrt(sum_j (r - mean)^2 / n) (population);

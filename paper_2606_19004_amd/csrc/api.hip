@@ -569,6 +569,26 @@ dit_status flow_step(float* x, const float* v, const float* noise, int64_t n, fl
   return DIT_OK;
 }
 
+dit_status flow_logprob(const float* x, const float* v, const float* x_next, int32_t batch, int64_t n_per_sample,
+                        float t, float t_next, float noise_level, double* logp, dit_stream stream) {
+  if (batch < 0 || n_per_sample < 0)
+    return fail(DIT_ERR_INVALID_ARG, "batch %d / n_per_sample %lld < 0", batch, (long long)n_per_sample);
+  if (!(noise_level > 0.f) || !std::isfinite(noise_level))
+    return fail(DIT_ERR_DOMAIN, "flow_logprob needs a finite noise_level > 0 (the ODE step has no density)");
+  if (!(t > 0.f && t < 1.f) || !std::isfinite(t_next) || !(t_next < t))
+    return fail(DIT_ERR_DOMAIN, "flow_logprob needs 0 < t < 1 and t_next < t (t=%g, t_next=%g)", t, t_next);
+  if (batch == 0) return DIT_OK;
+  if (!logp) return fail(DIT_ERR_INVALID_ARG, "logp NULL");
+  if (n_per_sample > 0 && (!x || !v || !x_next)) return fail(DIT_ERR_INVALID_ARG, "x/v/x_next NULL");
+  const double td = t, h = (double)t_next - td, a = noise_level;
+  const double var = a * a * td / (1.0 - td) * (-h);
+  const double k1 = 0.5 * a * a / (1.0 - td);           // sigma^2 / (2t)
+  const double cst = -0.5 * (double)n_per_sample * std::log(2.0 * M_PI * var);
+  TIMED("flow_logprob", 0, 12.0 * batch * n_per_sample, hs(stream),
+        flow_logprob_launch(x, v, x_next, batch, n_per_sample, h, k1, 1.0 - td, 0.5 / var, cst, logp, hs(stream)));
+  return DIT_OK;
+}
+
 dit_status group_reward_stats(const float* rewards, int32_t groups, int32_t n, float adv_eps, int32_t k_select,
                               float* mean, float* stdv, float* adv, int32_t* order, int32_t* selected,
                               dit_stream stream) {

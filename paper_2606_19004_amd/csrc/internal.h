@@ -113,6 +113,10 @@ hipError_t silu_f32(const float* in, float* out, int64_t n, hipStream_t s);
 hipError_t cast_f32_to_bf16(const float* in, u16* out, int64_t n, hipStream_t s);
 hipError_t timestep_sinusoid(const float* t_dev, float t_scalar, float* e, int B, hipStream_t s);
 hipError_t rope_table(float* tab, int npos, int head_dim, float theta, hipStream_t s);
+// per-sample Gaussian log-density of an SDE step: logp[b] = -sum (xn - mean)^2 * inv2var + cst,
+// mean = x + h (v + k1 (x + omt v))
+hipError_t flow_logprob_launch(const float* x, const float* v, const float* xn, int batch, int64_t n, double h,
+                               double k1, double omt, double inv2var, double cst, double* logp, hipStream_t s);
 hipError_t flow_update(float* x, const float* v, const float* noise, int64_t n,
                        float cx, float cv, float ce, hipStream_t s);
 hipError_t reward_stats(const float* r, int G, int n, float adv_eps, int k,

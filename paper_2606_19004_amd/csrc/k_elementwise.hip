@@ -1,5 +1,6 @@
 // Memory-bound and latency-bound kernels of the denoise step for gfx950:
 //   flow_update    fused Euler / SDE latent update (fp32, 16-byte vector access)
+//   flow_logprob   per-sample Gaussian log-density of an SDE step (fp64 sums)
 //   ln_modulate    LayerNorm (fp32 statistics) + adaLN modulate, one wave per row
 //   gemv           batched GEMV for the adaLN / timestep / final modulation vectors
 //   reward_stats   per prompt-group mean, std, advantages, stable descending ranks
@@ -58,6 +59,56 @@ __global__ void flow_update_scalar(float* x, const float* v, const float* e, int
     if (e) r = fmaf(ce, e[i], r);
     x[i] = r;
   }
+}
+
+// Log-density of an SDE step's output, one 1024-thread workgroup per sample: each thread sums
+// (x_next - mean)^2 over a strided share of the sample in fp64 (the mean too is formed in fp64
+// from the fp32 inputs), then the workgroup reduces in a fixed order.
+template <bool VEC>
+__global__ void __launch_bounds__(1024) flow_logprob_kernel(const float* __restrict__ x, const float* __restrict__ v,
+                                                            const float* __restrict__ xn, int64_t n, double h,
+                                                            double k1, double omt, double inv2var, double cst,
+                                                            double* __restrict__ logp) {
+  __shared__ double part[16];
+  const int64_t base = (int64_t)blockIdx.x * n;
+  double acc = 0.0;
+  auto term = [&](float xf, float vf, float nf) {
+    const double xd = xf, vd = vf;
+    const double mean = xd + h * (vd + k1 * (xd + omt * vd));
+    const double r = (double)nf - mean;
+    acc = fma(r, r, acc);
+  };
+  if (VEC) {
+    const float4* x4 = (const float4*)(x + base);
+    const float4* v4 = (const float4*)(v + base);
+    const float4* n4 = (const float4*)(xn + base);
+    for (int64_t i = threadIdx.x; i < n / 4; i += 1024) {
+      const float4 a = x4[i], b = v4[i], c = n4[i];
+      term(a.x, b.x, c.x);
+      term(a.y, b.y, c.y);
+      term(a.z, b.z, c.z);
+      term(a.w, b.w, c.w);
+    }
+  } else {
+    for (int64_t i = threadIdx.x; i < n; i += 1024) term(x[base + i], v[base + i], xn[base + i]);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o, 64);
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double s = 0.0;
+    for (int w = 0; w < 16; w++) s += part[w];
+    logp[blockIdx.x] = -s * inv2var + cst;
+  }
+}
+
+hipError_t flow_logprob_launch(const float* x, const float* v, const float* xn, int batch, int64_t n, double h,
+                               double k1, double omt, double inv2var, double cst, double* logp, hipStream_t s) {
+  const bool vec = n % 4 == 0 && ((uintptr_t)x | (uintptr_t)v | (uintptr_t)xn) % 16 == 0;
+  if (vec) flow_logprob_kernel<true><<<batch, 1024, 0, s>>>(x, v, xn, n, h, k1, omt, inv2var, cst, logp);
+  else flow_logprob_kernel<false><<<batch, 1024, 0, s>>>(x, v, xn, n, h, k1, omt, inv2var, cst, logp);
+  return hipGetLastError();
 }
 
 hipError_t flow_update(float* x, const float* v, const float* noise, int64_t n, float cx, float cv, float ce,

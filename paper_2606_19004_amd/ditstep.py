@@ -26,7 +26,7 @@ DIT_F32, DIT_BF16 = 0, 1
 STATUS = {0: "DIT_OK", 1: "DIT_ERR_INVALID_ARG", 2: "DIT_ERR_SHAPE", 3: "DIT_ERR_DOMAIN", 4: "DIT_ERR_NAN",
           5: "DIT_ERR_UNSUPPORTED", 6: "DIT_ERR_HIP", 7: "DIT_ERR_WORKSPACE"}
 EXPORTS = ("dit_abi_version", "dit_status_string", "dit_last_error_message", "dit_block_workspace_bytes",
-           "dit_block_forward", "dit_block_mlp", "joint_attention", "flow_step", "group_reward_stats",
+           "dit_block_forward", "dit_block_mlp", "joint_attention", "flow_step", "flow_logprob", "group_reward_stats",
            "dit_timestep_embed", "dit_patch_embed", "dit_final_layer", "dit_denoise_workspace_bytes",
            "dit_denoise_step", "dit_profile_begin", "dit_profile_end")
 
@@ -75,6 +75,7 @@ _sigs = {
     "joint_attention": ([_vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _i64, _i64, _i64, _i64, _i64, _i64, _f32, _i32,
                          _stream], _i32),
     "flow_step": ([_vp, _vp, _vp, _i64, _f32, _f32, _f32, _stream], _i32),
+    "flow_logprob": ([_vp, _vp, _vp, _i32, _i64, _f32, _f32, _f32, _vp, _stream], _i32),
     "group_reward_stats": ([_vp, _i32, _i32, _f32, _i32, _vp, _vp, _vp, _vp, _vp, _stream], _i32),
     "dit_timestep_embed": ([C.POINTER(BlockConfig), C.POINTER(StepWeights), _i32, _vp, _vp, _vp, _sz, _stream], _i32),
     "dit_patch_embed": ([C.POINTER(BlockConfig), C.POINTER(StepWeights), _i32, _i32, _vp, _vp, _vp, _sz, _stream], _i32),
@@ -180,6 +181,14 @@ def joint_attention(q, k, v, o, batch, heads, seq, head_dim, qkv_strides, o_stri
 
 def flow_step(x, v, noise, t, t_next, noise_level, stream=None):
     _check(_lib.flow_step(_ptr(x), _ptr(v), _ptr(noise), x.numel(), t, t_next, noise_level, _s(stream)))
+
+
+def flow_logprob(x, v, x_next, t, t_next, noise_level, logp, stream=None):
+    """x, v, x_next: [batch][n] fp32 device tensors (any trailing shape, flattened per sample);
+    logp: [batch] fp64 device tensor."""
+    b = x.shape[0] if x.dim() > 0 else 0
+    n = x.numel() // b if b else 0
+    _check(_lib.flow_logprob(_ptr(x), _ptr(v), _ptr(x_next), b, n, t, t_next, noise_level, _ptr(logp), _s(stream)))
 
 
 def group_reward_stats(rewards, adv_eps=1e-4, k_select=0, mean=None, std=None, adv=None, order=None, selected=None,

@@ -112,3 +112,55 @@ def test_reward_stats_constant_and_errors(d):
     with pytest.raises(d.DitError) as ei:
         d.group_reward_stats(dev(bad[:, :4]), 1e-4, 5, mean=mean)
     assert ei.value.name == "DIT_ERR_INVALID_ARG"
+
+
+# ----------------------------------------------------------------------------------------------
+# flow_logprob: the log-density of an SDE step's output under its Gaussian transition
+# ----------------------------------------------------------------------------------------------
+# The kernel forms the mean and the squared residuals in fp64 from the same fp32 inputs the oracle
+# reads, so the two differ only by summation order: ~1e-15 relative. 1e-10 leaves a wide margin and
+# still fails any wrong coefficient (a term of the mean or the variance off by one ulp of fp32 moves
+# a sum of 1e5 residuals by far more).
+TOL_LOGP = 1e-10
+
+
+@pytest.mark.parametrize("b,n", [(2, 4096), (16, 64 * 1024), (3, 1001), (1, 1), (5, 4)])
+@pytest.mark.parametrize("t,tn,a", [(0.73, 0.68, 0.7), (0.3, 0.05, 1.0)])
+def test_flow_logprob_matches_oracle(d, b, n, t, tn, a):
+    rng = np.random.default_rng(b * 1000 + n)
+    x, v, e = (rng.standard_normal((b, n)).astype(np.float32) for _ in range(3))
+    xd = dev(x)
+    d.flow_step(xd, dev(v), dev(e), t, tn, a)       # x_next drawn by the library's own SDE step
+    xn = xd.cpu().numpy()
+    logp = torch.zeros(b, dtype=torch.float64, device="cuda")
+    d.flow_logprob(dev(x), dev(v), dev(xn), t, tn, a, logp)
+    f = lambda z: float(np.float32(z))  # noqa: E731
+    ref = O.flow_logprob(x.astype(np.float64), v.astype(np.float64), xn.astype(np.float64), f(t), f(tn), f(a))
+    got = logp.cpu().numpy()
+    assert np.all(np.abs(got - ref) <= TOL_LOGP * np.abs(ref) + 1e-9), (got, ref)
+
+
+def test_flow_logprob_scalar_path_and_determinism(d):
+    rng = np.random.default_rng(9)
+    b, n = 4, 3000
+    x, v, xn = (rng.standard_normal((b, n)).astype(np.float32) for _ in range(3))
+    buf = dev(np.r_[np.float32(0), x.ravel()])
+    xo = buf[1:].view(b, n)                          # 4-byte offset: scalar path
+    out = [torch.zeros(b, dtype=torch.float64, device="cuda") for _ in range(2)]
+    for o in out:
+        d.flow_logprob(xo, dev(v), dev(xn), 0.6, 0.55, 0.7, o)
+    assert torch.equal(out[0], out[1])
+    ref = O.flow_logprob(x.astype(np.float64), v.astype(np.float64), xn.astype(np.float64), float(np.float32(0.6)),
+                         float(np.float32(0.55)), float(np.float32(0.7)))
+    got = out[0].cpu().numpy()
+    assert np.all(np.abs(got - ref) <= TOL_LOGP * np.abs(ref))
+
+
+def test_flow_logprob_domain_errors(d):
+    x = dev(np.ones((2, 64), np.float32))
+    logp = torch.full((2,), 7.0, dtype=torch.float64, device="cuda")
+    for args in [(0.5, 0.45, 0.0), (1.0, 0.95, 0.7), (0.0, -0.1, 0.7), (0.5, 0.5, 0.7), (0.5, 0.6, 0.7)]:
+        with pytest.raises(d.DitError) as ei:
+            d.flow_logprob(x, x, x, *args, logp)
+        assert ei.value.name == "DIT_ERR_DOMAIN"
+    assert torch.all(logp == 7.0)                   # nothing written
