@@ -2,7 +2,7 @@
 
     python -m paper_2606_19004_amd.build        # or build() from Python
 
-Each .hip under csrc/ compiles to an object under _build/ (in parallel), then
+Each .hip (and host-only .cpp) under csrc/ compiles to an object under _build/ (in parallel), then
 the objects link into paper_2606_19004_amd/libditstep.so.
 """
 from __future__ import annotations
@@ -29,6 +29,9 @@ HIPCC_FLAGS = [
 ]
 
 
+HOST_FLAGS = ["-x", "c++", "-O2", "-fPIC", "-std=c++17", "-Wall", "-I", os.path.join(ROOT, "include")]
+
+
 def hipcc() -> str:
     for cand in (os.environ.get("HIPCC"), "/opt/rocm/bin/hipcc", shutil.which("hipcc")):
         if cand and os.path.exists(cand):
@@ -46,8 +49,11 @@ def _run(cmd):
 def build(verbose: bool = False, jobs: int = 4) -> str:
     os.makedirs(OBJ, exist_ok=True)
     cc = hipcc()
-    srcs = sorted(f for f in os.listdir(CSRC) if f.endswith(".hip"))
-    cmds = [[cc, *HIPCC_FLAGS, "-c", os.path.join(CSRC, f), "-o", os.path.join(OBJ, f[:-4] + ".o")] for f in srcs]
+    # .hip: kernels and their host code; .cpp: host-only code (planner, seed bank), plain C++
+    srcs = sorted(f for f in os.listdir(CSRC) if f.endswith((".hip", ".cpp")))
+    objs = [os.path.join(OBJ, f.rsplit(".", 1)[0] + ".o") for f in srcs]
+    cmds = [[cc, *(HIPCC_FLAGS if f.endswith(".hip") else HOST_FLAGS), "-c", os.path.join(CSRC, f), "-o", o]
+            for f, o in zip(srcs, objs)]
     with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
         results = list(ex.map(_run, cmds))
     for cmd, (rc, out) in zip(cmds, results):
@@ -57,7 +63,7 @@ def build(verbose: bool = False, jobs: int = 4) -> str:
             raise RuntimeError(f"hipcc failed ({rc}) for {cmd[-3]}:\n{out}")
     tmp = LIB + ".tmp"
     rc, out = _run([cc, "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp,
-                    *[os.path.join(OBJ, f[:-4] + ".o") for f in srcs]])
+                    *objs])
     if rc != 0:
         raise RuntimeError(f"link failed:\n{out}")
     os.replace(tmp, LIB)

@@ -11,6 +11,7 @@
 
 #include "../../include/ditstep.h"
 #include "internal.h"
+#include "status.h"
 
 using namespace dit;
 
@@ -27,6 +28,20 @@ dit_status fail(dit_status s, const char* fmt, ...) {
   g_err = buf;
   return s;
 }
+
+}  // namespace
+
+dit_status dit::set_error(dit_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+namespace {
 
 #define HIP_TRY(expr)                                                                         \
   do {                                                                                        \
