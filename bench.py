@@ -276,6 +276,48 @@ def make_step(d, cfg, x):
     return step
 
 
+def next_rows(torch, d, cfg, x):
+    """Rows past the denoise step: the SDE step's log-density on this workload's latents (GPU,
+    timed with HIP events over 20 launches), and one planner iteration plus the seed-bank update
+    for this workload's reward groups (native host code, wall clock over 2000 iterations)."""
+    from paper_2606_19004_amd import planner as pn
+    out = {}
+    if cfg.noise_level > 0:
+        B = cfg.batch
+        logp = torch.empty(B, dtype=torch.float64, device="cuda")
+        d.flow_logprob(x.latent, x.v, x.latent, x.t, x.t_next, cfg.noise_level, logp)
+        torch.cuda.synchronize()
+        d.dit_profile_begin()
+        for _ in range(20):
+            d.flow_logprob(x.latent, x.v, x.latent, x.t, x.t_next, cfg.noise_level, logp)
+        st = [k for k in d.dit_profile_end() if k["name"] == "flow_logprob"][0]
+        avg = st["total_ms"] / st["launches"]
+        out["flow_logprob"] = {"avg_us": round(avg * 1e3, 2), "elements": x.latent.numel(),
+                               "gbs": round(st["bytes"] / (st["total_ms"] * 1e-3) / 1e9, 1),
+                               "frac_hbm": round(st["bytes"] / (st["total_ms"] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
+    pl = pn.Planner([4, 8, 16, 24, 32], [12, 14, 16, 18, 20], beta=0.5, window=10, prompts=32)
+    rng = np.random.default_rng(0)
+    fb = rng.uniform(0.8, 2.0, 2000).tolist()
+    spot = rng.integers(0, 12, 2000).tolist()
+    t0 = time.perf_counter()
+    for i in range(2000):
+        a, _, _ = pl.select(60.0, spot[i], 0.04)
+        pl.update(a, fb[i])
+    plan_us = (time.perf_counter() - t0) / 2000 * 1e6
+    G, n, k = max(cfg.reward_groups, 1), max(cfg.reward_n, 1), max(cfg.reward_k, 1)
+    bank = pn.SeedBank(k)
+    seeds = rng.integers(0, 2**40, (G, n)).tolist()
+    sel = x.selected.cpu().tolist() if cfg.reward_groups else [list(range(k))] * G
+    t0 = time.perf_counter()
+    for _ in range(200):
+        bank.put_selected(list(range(G)), seeds, sel)
+    bank_us = (time.perf_counter() - t0) / 200 * 1e6
+    out["planner"] = {"select_update_us": round(plan_us, 2), "actions": pl.num_actions,
+                      "seed_bank_put_us": round(bank_us, 2), "groups": G, "seeds_per_group": n, "k": k,
+                      "note": "host code, wall clock including the Python binding"}
+    return out
+
+
 def cpu_baseline(cfg, n_seeds):
     """Time the oracle on a bounded sample: one block for `n_seeds` seeds (all rows),
     scaled to a full step (blocks x K seeds). Block work dominates the step."""
@@ -368,6 +410,8 @@ def main():
     summary["attention_frac"] = (round(summary["attention_tflops"] / PEAK_BF16_TFLOPS, 4)
                                  if summary["attention_tflops"] else None)
 
+    extra = next_rows(torch, d, cfg, x)
+
     cpu = None
     if not args.no_cpu_baseline:
         print("timing the CPU oracle on a bounded sample ...", file=sys.stderr, flush=True)
@@ -385,6 +429,7 @@ def main():
         "roofline": roofline,
         "mfma_summary": summary,
         "kernels": kernels,
+        "next_rows": extra,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

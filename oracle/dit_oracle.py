@@ -352,3 +352,72 @@ def denoise_step(cfg, step_w, blocks_w, latent, x_txt, t, t_next, eps, a):
         x_img, x_txt = block_forward(cfg, w, temb, x_img, x_txt)
     v = final_layer(x_img, temb, step_w)
     return flow_step(latent, v, eps, t, t_next, a), v, temb
+
+
+# ---------------------------------------------------------------------------
+# TeaCache gate: skip the block stack on steps whose block input barely moved
+# ---------------------------------------------------------------------------
+# The exploration planner lowers the effective number of denoising steps s with TeaCache
+# (section 4.3.1): it caches the block stack's output residual and reuses it on steps whose
+# timestep-modulated input differs little from the previous step's. Readings (the paper
+# names TeaCache and does not restate it): the compared input is block 0's modulated image
+# input LN(x_img)(1 + scale1) + shift1; the distance is the relative L1 distance over the
+# whole batch, sum |h - h_prev| / sum |h_prev|; a caller-given polynomial rescales it
+# (identity when none is given: fitted coefficients are model-specific and not printed);
+# the rescaled distances accumulate across steps, and a step reuses the cached residual
+# while the accumulated value stays below the threshold, otherwise it runs the blocks and
+# the accumulator restarts at 0. The first step, and any step the caller forces (e.g. the
+# last one), runs the blocks. The K seeds of a batch skip or run together.
+def teacache_rel_l1(h_now, h_prev):
+    """sum |h_now - h_prev| / sum |h_prev| over all elements."""
+    h_now = np.asarray(h_now, dtype=np.float64)
+    h_prev = np.asarray(h_prev, dtype=np.float64)
+    return float(np.abs(h_now - h_prev).sum() / np.abs(h_prev).sum())
+
+
+class TeaCacheState:
+    def __init__(self, threshold, coef=()):
+        self.threshold = float(threshold)
+        self.coef = [float(c) for c in coef]     # highest power first; empty = identity
+        self.accumulated = 0.0
+        self.h_prev = None                       # block 0's modulated image input of the last step
+        self.residual = None                     # x_img after the blocks minus before, last computed step
+
+    def gate(self, rel, force=False):
+        """True: run the blocks; False: reuse the cached residual. Updates the accumulator."""
+        if force or self.h_prev is None or self.residual is None:
+            self.accumulated = 0.0
+            return True
+        self.accumulated += float(np.polyval(self.coef, rel)) if self.coef else rel
+        if self.accumulated < self.threshold:
+            return False
+        self.accumulated = 0.0
+        return True
+
+
+def block0_modulated_input(w0, temb, x_img):
+    """LN(x_img)(1 + scale1) + shift1 with block 0's image-stream modulation, [B][N_i][D]."""
+    m = modulation(temb, w0["img"]["mod_w"], w0["img"]["mod_b"])
+    return modulate(x_img, m["shift1"], m["scale1"])
+
+
+def denoise_step_teacache(cfg, step_w, blocks_w, latent, x_txt, t, t_next, eps, a, state, force=False):
+    """denoise_step with the TeaCache gate in front of the block stack.
+
+    Returns (latent', v, ran_blocks, rel) with rel = None on a step without a previous input."""
+    b = latent.shape[0]
+    temb = timestep_embed(np.full(b, t), step_w)
+    x_img = patch_embed(latent, step_w)
+    h0 = block0_modulated_input(blocks_w[0], temb, x_img) if blocks_w else x_img
+    rel = teacache_rel_l1(h0, state.h_prev) if state.h_prev is not None else None
+    run = state.gate(rel, force)
+    state.h_prev = h0
+    if run:
+        x_in = x_img
+        for w in blocks_w:
+            x_img, x_txt = block_forward(cfg, w, temb, x_img, x_txt)
+        state.residual = x_img - x_in
+    else:
+        x_img = x_img + state.residual
+    v = final_layer(x_img, temb, step_w)
+    return flow_step(latent, v, eps, t, t_next, a), v, run, rel
