@@ -244,6 +244,50 @@ dit_status dit_denoise_step(const dit_block_config* cfg, const dit_step_weights*
                             float* v_out, void* workspace, size_t workspace_bytes, dit_stream stream);
 
 /* ------------------------------------------------------------------ */
+/* TeaCache gate (fewer effective denoising steps, section 4.3.1)       */
+/* ------------------------------------------------------------------ */
+/* The exploration planner's effective step count s comes from TeaCache: the block stack's
+ * output residual is cached and reused on steps whose block input barely moved. Here:
+ *   h    = block 0's modulated image input LN(x_img)(1 + scale1) + shift1, [B][N_i][D];
+ *   rel  = sum |h - h_prev| / sum |h_prev| over the whole batch (the K seeds of a batch
+ *          run or skip together);
+ *   acc += poly(rel), poly = coef[0] rel^(n-1) + ... + coef[n-1] (identity when n_coef == 0);
+ *   the step reuses the residual while acc < threshold, else runs the blocks and acc = 0.
+ * The first step of a state (no h_prev or no residual yet) and any step with force != 0
+ * (e.g. the last) run the blocks and reset acc. Initialise a state with
+ * dit_teacache_init; the caller owns it (host memory). */
+typedef struct {
+  double threshold;
+  int32_t n_coef;          /* 0..8 */
+  double coef[8];          /* rescale polynomial, highest power first */
+  double accumulated;
+  int32_t has_prev;        /* the cache holds h of an earlier step */
+  int32_t has_residual;    /* the cache holds the residual of an earlier computed step */
+} dit_teacache_state;
+
+/* threshold >= 0, 0 <= n_coef <= 8 (coef may be NULL when n_coef == 0). */
+dit_status dit_teacache_init(dit_teacache_state* st, double threshold, const double* coef, int32_t n_coef);
+/* The gate alone (host): *run_blocks = 1 to run the blocks, 0 to reuse the residual; rel is
+ * ignored when the state has no previous input or force != 0. */
+dit_status dit_teacache_gate(dit_teacache_state* st, double rel, int32_t force, int32_t* run_blocks);
+/* Device cache for one state: h_prev [B][N_i][D] (config dtype), residual [B][N_i][D] fp32 and
+ * reduction scratch. 0 for an invalid config. */
+size_t dit_teacache_cache_bytes(const dit_block_config* cfg, int32_t batch);
+/* dit_denoise_step with the gate in front of the block stack (same arguments and workspace,
+ * n_blocks >= 1). Computes h, updates the cache's h_prev, and either runs the blocks (then
+ * stores the residual x_out - x_in) or adds the stored residual to the patch-embedded input.
+ * *ran_blocks (may be NULL) receives the decision and *rel (may be NULL) the distance (NaN on
+ * a step without a previous input). The decision needs the distance on the host, so the call
+ * synchronises `stream` once. DIT_ERR_WORKSPACE if cache_bytes is too small. */
+dit_status dit_denoise_step_teacache(const dit_block_config* cfg, const dit_step_weights* sw,
+                                     const dit_block_weights* blocks, int32_t n_blocks, int32_t batch,
+                                     int32_t latent_dim, float t, float t_next, float noise_level,
+                                     float* latent, const void* x_txt, const float* noise, float* v_out,
+                                     dit_teacache_state* state, int32_t force, void* cache,
+                                     size_t cache_bytes, int32_t* ran_blocks, double* rel,
+                                     void* workspace, size_t workspace_bytes, dit_stream stream);
+
+/* ------------------------------------------------------------------ */
 /* kernel timing (benchmark instrumentation)                            */
 /* ------------------------------------------------------------------ */
 /* One kernel class (a family of launches: "gemm_mlp_up_gelu", "attention",

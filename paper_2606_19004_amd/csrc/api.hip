@@ -4,6 +4,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <limits>
 #include <map>
 #include <mutex>
 #include <string>
@@ -702,6 +703,151 @@ dit_status dit_denoise_step(const dit_block_config* c, const dit_step_weights* s
   size_t inner_bytes = workspace_bytes - L.inner;
   for (int i = 0; i < n_blocks; i++)
     if ((st = dit_block_forward(c, &blocks[i], B, temb, ximg, xtxt, inner, inner_bytes, stream))) return st;
+  if ((st = run_final(c, sw, B, C, temb, ximg, v, inner, s))) return st;
+  TIMED("flow_step", 0, (noise_level > 0.f ? 16.0 : 12.0) * B * c->n_img * C, s,
+        flow_update(latent, v, noise_level > 0.f ? noise : nullptr, (int64_t)B * c->n_img * C, cx, cv, ce, s));
+  return DIT_OK;
+}
+
+// ---- TeaCache gate ----
+namespace {
+struct TeaCacheLayout {
+  size_t hprev, resid, parts, sums, total;
+};
+TeaCacheLayout teacache_layout(const dit_block_config* c, int64_t B) {
+  auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
+  const size_t n = (size_t)B * c->n_img * c->hidden;
+  TeaCacheLayout L{};
+  L.hprev = 0;
+  L.resid = up(n * esize(c->dtype));
+  L.parts = L.resid + up(n * 4);
+  L.sums = L.parts + up(2 * sizeof(double) * TEACACHE_PARTS);
+  L.total = L.sums + 256;
+  return L;
+}
+}  // namespace
+
+dit_status dit_teacache_init(dit_teacache_state* st, double threshold, const double* coef, int32_t n_coef) {
+  if (!st) return fail(DIT_ERR_INVALID_ARG, "state is NULL");
+  if (!(threshold >= 0.0) || !std::isfinite(threshold)) return fail(DIT_ERR_INVALID_ARG, "threshold %g < 0", threshold);
+  if (n_coef < 0 || n_coef > 8 || (n_coef > 0 && !coef)) return fail(DIT_ERR_INVALID_ARG, "n_coef %d (0..8)", n_coef);
+  std::memset(st, 0, sizeof *st);
+  st->threshold = threshold;
+  st->n_coef = n_coef;
+  for (int i = 0; i < n_coef; i++) {
+    if (!std::isfinite(coef[i])) return fail(DIT_ERR_INVALID_ARG, "coef[%d] not finite", i);
+    st->coef[i] = coef[i];
+  }
+  return DIT_OK;
+}
+
+dit_status dit_teacache_gate(dit_teacache_state* st, double rel, int32_t force, int32_t* run_blocks) {
+  if (!st || !run_blocks) return fail(DIT_ERR_INVALID_ARG, "state / run_blocks is NULL");
+  if (st->n_coef < 0 || st->n_coef > 8) return fail(DIT_ERR_INVALID_ARG, "state n_coef %d (0..8)", st->n_coef);
+  if (force || !st->has_prev || !st->has_residual) {
+    st->accumulated = 0.0;
+    *run_blocks = 1;
+    return DIT_OK;
+  }
+  if (!std::isfinite(rel)) return fail(DIT_ERR_NAN, "distance %g is not finite", rel);
+  double v = rel;
+  if (st->n_coef > 0) {   // Horner, highest power first
+    v = 0.0;
+    for (int i = 0; i < st->n_coef; i++) v = v * rel + st->coef[i];
+  }
+  st->accumulated += v;
+  if (st->accumulated < st->threshold) {
+    *run_blocks = 0;
+  } else {
+    st->accumulated = 0.0;
+    *run_blocks = 1;
+  }
+  return DIT_OK;
+}
+
+size_t dit_teacache_cache_bytes(const dit_block_config* c, int32_t batch) {
+  if (check_config(c) != DIT_OK || batch < 0) return 0;
+  return teacache_layout(c, batch).total;
+}
+
+dit_status dit_denoise_step_teacache(const dit_block_config* c, const dit_step_weights* sw,
+                                     const dit_block_weights* blocks, int32_t n_blocks, int32_t batch,
+                                     int32_t latent_dim, float t, float t_next, float noise_level, float* latent,
+                                     const void* x_txt, const float* noise, float* v_out, dit_teacache_state* state,
+                                     int32_t force, void* cache, size_t cache_bytes, int32_t* ran_blocks, double* rel,
+                                     void* workspace, size_t workspace_bytes, dit_stream stream) {
+  dit_status st = check_config(c);
+  if (st || (st = check_step_weights(sw))) return st;
+  if (n_blocks < 1 || !blocks) return fail(DIT_ERR_INVALID_ARG, "the gated step needs n_blocks >= 1");
+  if (!state) return fail(DIT_ERR_INVALID_ARG, "state is NULL");
+  if (batch < 0) return fail(DIT_ERR_INVALID_ARG, "batch < 0");
+  if (latent_dim <= 0 || latent_dim % 64) return fail(DIT_ERR_UNSUPPORTED, "latent_dim %d (multiple of 64)", latent_dim);
+  float cx, cv, ce;
+  if ((st = flow_coefficients(t, t_next, noise_level, noise != nullptr, &cx, &cv, &ce))) return st;
+  if (batch == 0) return DIT_OK;
+  if (!latent || !aligned16(latent) || (c->n_txt > 0 && (!x_txt || !aligned16(x_txt))) ||
+      (v_out && !aligned16(v_out)))
+    return fail(DIT_ERR_INVALID_ARG, "latent/x_txt/v_out NULL or not 16-byte aligned");
+  const TeaCacheLayout TL = teacache_layout(c, batch);
+  if (!cache || !aligned16(cache) || cache_bytes < TL.total)
+    return fail(DIT_ERR_WORKSPACE, "cache %zu bytes < %zu or not aligned", cache_bytes, TL.total);
+  StepWs L = step_layout(c, batch, latent_dim);
+  if ((st = check_ws(workspace, workspace_bytes, L.total))) return st;
+  char* ws = (char*)workspace;
+  float* temb = (float*)(ws + L.temb);
+  void* ximg = ws + L.ximg;
+  void* xtxt = ws + L.xtxt;
+  float* v = v_out ? v_out : (float*)(ws + L.v);
+  char* inner = ws + L.inner;
+  for (int i = 0; i < n_blocks; i++)
+    if ((st = check_block_args(c, &blocks[i], batch, temb, ximg, xtxt))) return st;
+  hipStream_t s = hs(stream);
+  const int B = batch, C = latent_dim, D = c->hidden;
+  const int64_t n_act = (int64_t)B * c->n_img * D;
+  char* cb = (char*)cache;
+  float* resid = (float*)(cb + TL.resid);
+  double* parts = (double*)(cb + TL.parts);
+  double* sums = (double*)(cb + TL.sums);
+  if ((st = run_timestep(c, sw, B, nullptr, t, temb, inner, s))) return st;
+  if ((st = run_patch(c, sw, B, C, latent, ximg, inner, s))) return st;
+  if (c->n_txt > 0)
+    HIP_TRY(hipMemcpyAsync(xtxt, x_txt, (size_t)B * c->n_txt * D * esize(c->dtype), hipMemcpyDeviceToDevice, s));
+  // block 0's modulated input: its modulation GEMV and pre-attention LN (both streams; the
+  // image rows are compared), in the block workspace the first block will overwrite
+  const BlockWs BL = block_layout(c, B);
+  if ((st = check_ws(inner, workspace_bytes - L.inner, BL.total))) return st;
+  if ((st = run_modulation(c, &blocks[0], B, temb, inner, BL, s))) return st;
+  if ((st = run_ln(c, B, ximg, xtxt, inner, BL, 0, D, s))) return st;
+  const bool measure = state->has_prev != 0;
+  TIMED("teacache_distance", 0, (measure ? 3.0 : 2.0) * n_act * esize(c->dtype), s,
+        teacache_distance(inner + BL.h, cb + TL.hprev, B, c->n_img, c->n_txt, D, measure, parts, sums, c->dtype, s));
+  double r = std::numeric_limits<double>::quiet_NaN();
+  if (measure) {
+    double hsums[2];
+    HIP_TRY(hipMemcpyAsync(hsums, sums, sizeof hsums, hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    r = hsums[1] > 0.0 ? hsums[0] / hsums[1] : (hsums[0] > 0.0 ? std::numeric_limits<double>::infinity() : 0.0);
+  }
+  int32_t run = 1;
+  if (measure && !std::isfinite(r)) {
+    run = 1;                 // a zero cached input: no meaningful distance, run the blocks
+    state->accumulated = 0.0;
+  } else if ((st = dit_teacache_gate(state, r, force, &run))) {
+    return st;
+  }
+  state->has_prev = 1;
+  if (run) {
+    TIMED("small_elementwise", 0, 0, s, teacache_residual(ximg, resid, n_act, 0, c->dtype, s));
+    size_t inner_bytes = workspace_bytes - L.inner;
+    for (int i = 0; i < n_blocks; i++)
+      if ((st = dit_block_forward(c, &blocks[i], B, temb, ximg, xtxt, inner, inner_bytes, stream))) return st;
+    TIMED("small_elementwise", 0, 0, s, teacache_residual(ximg, resid, n_act, 1, c->dtype, s));
+    state->has_residual = 1;
+  } else {
+    TIMED("small_elementwise", 0, 0, s, teacache_residual(ximg, resid, n_act, 2, c->dtype, s));
+  }
+  if (ran_blocks) *ran_blocks = run;
+  if (rel) *rel = r;
   if ((st = run_final(c, sw, B, C, temb, ximg, v, inner, s))) return st;
   TIMED("flow_step", 0, (noise_level > 0.f ? 16.0 : 12.0) * B * c->n_img * C, s,
         flow_update(latent, v, noise_level > 0.f ? noise : nullptr, (int64_t)B * c->n_img * C, cx, cv, ce, s));

@@ -25,6 +25,30 @@ template <> __device__ __forceinline__ u16 from_f32<u16>(float x) {
   return __builtin_bit_cast(u16, (__bf16)x);  // round to nearest even (v_cvt_pk_bf16_f32)
 }
 
+// four consecutive elements as fp32 (16-byte aligned for fp32, 8-byte for bf16), and back
+template <typename T> __device__ __forceinline__ void load4(const T* p, float* f);
+template <> __device__ __forceinline__ void load4<u16>(const u16* p, float* f) {
+  uint2 u = *(const uint2*)p;
+  f[0] = __uint_as_float(u.x << 16);
+  f[1] = __uint_as_float(u.x & 0xffff0000u);
+  f[2] = __uint_as_float(u.y << 16);
+  f[3] = __uint_as_float(u.y & 0xffff0000u);
+}
+template <> __device__ __forceinline__ void load4<float>(const float* p, float* f) {
+  float4 a = *(const float4*)p;
+  f[0] = a.x; f[1] = a.y; f[2] = a.z; f[3] = a.w;
+}
+template <typename T> __device__ __forceinline__ void store4(T* p, const float* f);
+template <> __device__ __forceinline__ void store4<u16>(u16* p, const float* f) {
+  uint2 u;
+  u.x = (uint32_t)from_f32<u16>(f[0]) | ((uint32_t)from_f32<u16>(f[1]) << 16);
+  u.y = (uint32_t)from_f32<u16>(f[2]) | ((uint32_t)from_f32<u16>(f[3]) << 16);
+  *(uint2*)p = u;
+}
+template <> __device__ __forceinline__ void store4<float>(float* p, const float* f) {
+  *(float4*)p = make_float4(f[0], f[1], f[2], f[3]);
+}
+
 // ---------------------------------------------------------------------------
 // row addressing: logical row m of a [rows][cols] operand lives at element
 //   (m / rows_per_batch) * batch_stride + (m % rows_per_batch) * row_stride + offset
@@ -117,6 +141,14 @@ hipError_t rope_table(float* tab, int npos, int head_dim, float theta, hipStream
 // mean = x + h (v + k1 (x + omt v))
 hipError_t flow_logprob_launch(const float* x, const float* v, const float* xn, int batch, int64_t n, double h,
                                double k1, double omt, double inv2var, double cst, double* logp, hipStream_t s);
+// TeaCache: per-block partial sums of |h - h_prev| and |h_prev| over the image rows of the joint
+// buffer h ([B][S][D], image rows at offset n_txt) against h_prev ([B][N_i][D]), summed in a fixed
+// order into sums[2] (skipped when !measure); h_prev is then overwritten with h.
+hipError_t teacache_distance(const void* h, void* h_prev, int B, int n_img, int n_txt, int D, bool measure,
+                             double* partials, double* sums, int dtype, hipStream_t s);
+// residual r (fp32) of the activation x (n elements): mode 0 r = x, 1 r = x - r, 2 x = x + r
+hipError_t teacache_residual(void* x, float* r, int64_t n, int mode, int dtype, hipStream_t s);
+constexpr int TEACACHE_PARTS = 512;
 hipError_t flow_update(float* x, const float* v, const float* noise, int64_t n,
                        float cx, float cv, float ce, hipStream_t s);
 hipError_t reward_stats(const float* r, int G, int n, float adv_eps, int k,

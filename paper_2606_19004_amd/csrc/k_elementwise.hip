@@ -111,6 +111,110 @@ hipError_t flow_logprob_launch(const float* x, const float* v, const float* xn, 
   return hipGetLastError();
 }
 
+// TeaCache distance: each thread walks 8-element chunks of the image rows (grid-stride), sums
+// |h - h_prev| and |h_prev| in fp64, and refreshes h_prev; one partial pair per workgroup.
+template <typename T>
+__global__ void __launch_bounds__(256) teacache_distance_kernel(const T* __restrict__ h, T* __restrict__ hp,
+                                                                int64_t chunks, int64_t per_b, int n_txt, int S,
+                                                                int D, int measure, double* __restrict__ part) {
+  __shared__ double sd[4], sp[4];
+  double ad = 0.0, ap = 0.0;
+  for (int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x; q < chunks; q += (int64_t)gridDim.x * 256) {
+    const int64_t e = q * 8, b = e / per_b, rem = e - b * per_b;
+    const int64_t r = rem / D, c = rem - r * D;
+    const T* src = h + (b * S + n_txt + r) * D + c;
+    float a[8], p[8];
+    load4<T>(src, a);
+    load4<T>(src + 4, a + 4);
+    if (measure) {
+      load4<T>(hp + e, p);
+      load4<T>(hp + e + 4, p + 4);
+#pragma unroll
+      for (int j = 0; j < 8; j++) {
+        ad += fabs((double)a[j] - (double)p[j]);
+        ap += fabs((double)p[j]);
+      }
+    }
+    store4<T>(hp + e, a);
+    store4<T>(hp + e + 4, a + 4);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    ad += __shfl_xor(ad, o, 64);
+    ap += __shfl_xor(ap, o, 64);
+  }
+  if ((threadIdx.x & 63) == 0) {
+    sd[threadIdx.x >> 6] = ad;
+    sp[threadIdx.x >> 6] = ap;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    part[2 * blockIdx.x] = sd[0] + sd[1] + sd[2] + sd[3];
+    part[2 * blockIdx.x + 1] = sp[0] + sp[1] + sp[2] + sp[3];
+  }
+}
+
+__global__ void teacache_sum_kernel(const double* __restrict__ part, int nparts, double* __restrict__ sums) {
+  if (threadIdx.x == 0) {
+    double a = 0.0, b = 0.0;
+    for (int i = 0; i < nparts; i++) {
+      a += part[2 * i];
+      b += part[2 * i + 1];
+    }
+    sums[0] = a;
+    sums[1] = b;
+  }
+}
+
+hipError_t teacache_distance(const void* h, void* h_prev, int B, int n_img, int n_txt, int D, bool measure,
+                             double* partials, double* sums, int dtype, hipStream_t s) {
+  const int64_t per_b = (int64_t)n_img * D, chunks = B * per_b / 8;
+  if (chunks == 0) return hipSuccess;
+  const int grid = (int)std::min<int64_t>(TEACACHE_PARTS, cdiv(chunks, (int64_t)256));
+  const int S = n_img + n_txt;
+  if (dtype == DT_BF16)
+    teacache_distance_kernel<u16><<<grid, 256, 0, s>>>((const u16*)h, (u16*)h_prev, chunks, per_b, n_txt, S, D,
+                                                       measure, partials);
+  else
+    teacache_distance_kernel<float><<<grid, 256, 0, s>>>((const float*)h, (float*)h_prev, chunks, per_b, n_txt, S,
+                                                         D, measure, partials);
+  if (measure) teacache_sum_kernel<<<1, 64, 0, s>>>(partials, grid, sums);
+  return hipGetLastError();
+}
+
+template <typename T, int MODE>
+__global__ void __launch_bounds__(256) teacache_residual_kernel(T* __restrict__ x, float* __restrict__ r, int64_t n4) {
+  for (int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x; q < n4; q += (int64_t)gridDim.x * 256) {
+    float a[4];
+    load4<T>(x + 4 * q, a);
+    float4 rv = MODE == 0 ? make_float4(0.f, 0.f, 0.f, 0.f) : *(const float4*)(r + 4 * q);
+    if (MODE == 0) {
+      *(float4*)(r + 4 * q) = make_float4(a[0], a[1], a[2], a[3]);
+    } else if (MODE == 1) {
+      *(float4*)(r + 4 * q) = make_float4(a[0] - rv.x, a[1] - rv.y, a[2] - rv.z, a[3] - rv.w);
+    } else {
+      float o[4] = {a[0] + rv.x, a[1] + rv.y, a[2] + rv.z, a[3] + rv.w};
+      store4<T>(x + 4 * q, o);
+    }
+  }
+}
+
+hipError_t teacache_residual(void* x, float* r, int64_t n, int mode, int dtype, hipStream_t s) {
+  const int64_t n4 = n / 4;
+  if (n4 == 0) return hipSuccess;
+  const int grid = (int)std::min<int64_t>(2048, cdiv(n4, (int64_t)256));
+  if (dtype == DT_BF16) {
+    if (mode == 0) teacache_residual_kernel<u16, 0><<<grid, 256, 0, s>>>((u16*)x, r, n4);
+    else if (mode == 1) teacache_residual_kernel<u16, 1><<<grid, 256, 0, s>>>((u16*)x, r, n4);
+    else teacache_residual_kernel<u16, 2><<<grid, 256, 0, s>>>((u16*)x, r, n4);
+  } else {
+    if (mode == 0) teacache_residual_kernel<float, 0><<<grid, 256, 0, s>>>((float*)x, r, n4);
+    else if (mode == 1) teacache_residual_kernel<float, 1><<<grid, 256, 0, s>>>((float*)x, r, n4);
+    else teacache_residual_kernel<float, 2><<<grid, 256, 0, s>>>((float*)x, r, n4);
+  }
+  return hipGetLastError();
+}
+
 hipError_t flow_update(float* x, const float* v, const float* noise, int64_t n, float cx, float cv, float ce,
                        hipStream_t s) {
   if (n <= 0) return hipSuccess;

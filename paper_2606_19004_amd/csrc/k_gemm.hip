@@ -36,28 +36,6 @@ __device__ __forceinline__ float gelu_tanh_f(float z) {
   return z * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-u2 * 1.4426950408889634f));
 }
 
-template <typename T> __device__ __forceinline__ void load4(const T* p, float* f);
-template <> __device__ __forceinline__ void load4<u16>(const u16* p, float* f) {
-  uint2 u = *(const uint2*)p;
-  f[0] = __uint_as_float(u.x << 16);
-  f[1] = __uint_as_float(u.x & 0xffff0000u);
-  f[2] = __uint_as_float(u.y << 16);
-  f[3] = __uint_as_float(u.y & 0xffff0000u);
-}
-template <> __device__ __forceinline__ void load4<float>(const float* p, float* f) {
-  float4 a = *(const float4*)p;
-  f[0] = a.x; f[1] = a.y; f[2] = a.z; f[3] = a.w;
-}
-template <typename T> __device__ __forceinline__ void store4(T* p, const float* f);
-template <> __device__ __forceinline__ void store4<u16>(u16* p, const float* f) {
-  uint2 u;
-  u.x = (uint32_t)from_f32<u16>(f[0]) | ((uint32_t)from_f32<u16>(f[1]) << 16);
-  u.y = (uint32_t)from_f32<u16>(f[2]) | ((uint32_t)from_f32<u16>(f[3]) << 16);
-  *(uint2*)p = u;
-}
-template <> __device__ __forceinline__ void store4<float>(float* p, const float* f) {
-  *(float4*)p = make_float4(f[0], f[1], f[2], f[3]);
-}
 
 // Per-row epilogue state, computed once per output row m.
 struct RowEpi {

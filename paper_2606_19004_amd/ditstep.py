@@ -28,7 +28,8 @@ STATUS = {0: "DIT_OK", 1: "DIT_ERR_INVALID_ARG", 2: "DIT_ERR_SHAPE", 3: "DIT_ERR
 EXPORTS = ("dit_abi_version", "dit_status_string", "dit_last_error_message", "dit_block_workspace_bytes",
            "dit_block_forward", "dit_block_mlp", "joint_attention", "flow_step", "flow_logprob", "group_reward_stats",
            "dit_timestep_embed", "dit_patch_embed", "dit_final_layer", "dit_denoise_workspace_bytes",
-           "dit_denoise_step", "dit_profile_begin", "dit_profile_end")
+           "dit_denoise_step", "dit_profile_begin", "dit_profile_end", "dit_teacache_init", "dit_teacache_gate",
+           "dit_teacache_cache_bytes", "dit_denoise_step_teacache")
 
 
 class DitError(RuntimeError):
@@ -55,6 +56,11 @@ class BlockWeights(C.Structure):
 
 class StepWeights(C.Structure):
     _fields_ = [(n, C.c_void_p) for n in _STEP_TENSORS]
+
+
+class TeaCacheState(C.Structure):
+    _fields_ = [("threshold", C.c_double), ("n_coef", C.c_int32), ("coef", C.c_double * 8),
+                ("accumulated", C.c_double), ("has_prev", C.c_int32), ("has_residual", C.c_int32)]
 
 
 class KernelStat(C.Structure):
@@ -85,6 +91,12 @@ _sigs = {
     "dit_denoise_step": ([C.POINTER(BlockConfig), C.POINTER(StepWeights), C.POINTER(BlockWeights), _i32, _i32, _i32,
                           _f32, _f32, _f32, _vp, _vp, _vp, _vp, _vp, _sz, _stream], _i32),
     "dit_profile_begin": ([], _i32),
+    "dit_teacache_init": ([C.POINTER(TeaCacheState), C.c_double, C.POINTER(C.c_double), _i32], _i32),
+    "dit_teacache_gate": ([C.POINTER(TeaCacheState), C.c_double, _i32, C.POINTER(_i32)], _i32),
+    "dit_teacache_cache_bytes": ([C.POINTER(BlockConfig), _i32], _sz),
+    "dit_denoise_step_teacache": ([C.POINTER(BlockConfig), C.POINTER(StepWeights), C.POINTER(BlockWeights), _i32,
+                                   _i32, _i32, _f32, _f32, _f32, _vp, _vp, _vp, _vp, C.POINTER(TeaCacheState), _i32,
+                                   _vp, _sz, C.POINTER(_i32), C.POINTER(C.c_double), _vp, _sz, _stream], _i32),
     "dit_profile_end": ([C.POINTER(KernelStat), _i32, C.POINTER(_i32)], _i32),
 }
 for _name, (_args, _res) in _sigs.items():
@@ -222,6 +234,36 @@ def dit_denoise_step(cfg, sw, blocks, t, t_next, noise_level, latent, x_txt, noi
     _check(_lib.dit_denoise_step(C.byref(cfg), C.byref(sw), arr, len(blocks), latent.shape[0], latent.shape[-1],
                                  t, t_next, noise_level, _ptr(latent), _ptr(x_txt), _ptr(noise), _ptr(v_out),
                                  _ptr(ws), ws.numel(), _s(stream)))
+
+
+def teacache_state(threshold, coef=()):
+    st = TeaCacheState()
+    c = (C.c_double * max(len(coef), 1))(*[float(x) for x in coef])
+    _check(_lib.dit_teacache_init(C.byref(st), float(threshold), c, len(coef)))
+    return st
+
+
+def dit_teacache_gate(state, rel, force=False):
+    run = _i32()
+    _check(_lib.dit_teacache_gate(C.byref(state), float(rel), int(bool(force)), C.byref(run)))
+    return bool(run.value)
+
+
+def dit_teacache_cache_bytes(cfg, batch):
+    return _lib.dit_teacache_cache_bytes(C.byref(cfg), batch)
+
+
+def dit_denoise_step_teacache(cfg, sw, blocks, t, t_next, noise_level, latent, x_txt, noise, v_out, state, cache, ws,
+                              force=False, stream=None):
+    """Returns (ran_blocks, rel)."""
+    arr = (BlockWeights * max(len(blocks), 1))(*blocks)
+    ran, rel = _i32(), C.c_double()
+    _check(_lib.dit_denoise_step_teacache(C.byref(cfg), C.byref(sw), arr, len(blocks), latent.shape[0],
+                                          latent.shape[-1], t, t_next, noise_level, _ptr(latent), _ptr(x_txt),
+                                          _ptr(noise), _ptr(v_out), C.byref(state), int(bool(force)), _ptr(cache),
+                                          cache.numel(), C.byref(ran), C.byref(rel), _ptr(ws), ws.numel(),
+                                          _s(stream)))
+    return bool(ran.value), rel.value
 
 
 def dit_profile_begin():
