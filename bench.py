@@ -344,6 +344,83 @@ def next_rows(torch, d, cfg, x):
     return out
 
 
+def other_configs(torch, d):
+    """The single-block configurations at their launch shapes, measured after the headline step:
+    512^2 block (K=8), 1280^2 block (K=4, joint attention over 6912 tokens), and one sequence-
+    parallel rank's share at 1280^2 (6 of 24 heads over 6912 tokens, K=8; MLP on a 1600 + 128 token
+    slice, K=8). Per configuration: ms per call (HIP events, median of 5 after 2 warm-ups) and the
+    GEMM / attention throughput of one instrumented call."""
+    out = {}
+    g = torch.Generator(device="cuda")
+    g.manual_seed(si.MASTER_SEED)
+
+    def w(shape, std=0.02):
+        return (torch.randn(shape, generator=g, device="cuda", dtype=torch.float32) * std).to(torch.bfloat16)
+
+    def timed(fn):
+        for _ in range(2):
+            fn()
+        ts = []
+        for _ in range(5):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn()
+            b.record()
+            b.synchronize()
+            ts.append(a.elapsed_time(b))
+        d.dit_profile_begin()
+        fn()
+        st = {k["name"]: k for k in d.dit_profile_end()}
+        return sorted(ts)[2], st
+
+    def frac(st, names):
+        ks = [st[n] for n in names if n in st]
+        fl, ms = sum(k["flops"] for k in ks), sum(k["total_ms"] for k in ks)
+        tf = fl / (ms * 1e-3) / 1e12 if ms else 0.0
+        return {"tflops": round(tf, 1), "frac": round(tf / PEAK_BF16_TFLOPS, 4), "ms": round(ms, 3)}
+
+    gemms = ["gemm_qkv_rope", "gemm_out_gate", "gemm_mlp_up_gelu", "gemm_mlp_down_gate"]
+    for name in ("block_512", "block_1280"):
+        cfg = si.CONFIGS[name]
+        bw = {s: {t: w(shp) for t, shp in si.block_weight_shapes(cfg).items()} for s in si.STREAMS}
+        blk = d.block_weights(bw["img"], bw["txt"])
+        c = d.block_config(cfg.hidden, cfg.heads, cfg.head_dim, cfg.mlp_hidden, cfg.n_img, cfg.n_txt, cfg.grid_h,
+                           cfg.grid_w, rope=cfg.rope, dtype=cfg.dtype)
+        B = cfg.batch
+        temb = torch.randn((B, cfg.hidden), generator=g, device="cuda")
+        xi = torch.randn((B, cfg.n_img, cfg.hidden), generator=g, device="cuda").to(torch.bfloat16)
+        xt = torch.randn((B, cfg.n_txt, cfg.hidden), generator=g, device="cuda").to(torch.bfloat16)
+        ws = d.workspace(d.dit_block_workspace_bytes(c, B))
+        ms, st = timed(lambda: d.dit_block_forward(c, blk, temb, xi, xt, ws))
+        out[name] = {"ms_per_block": round(ms, 3), "K": B, "tokens": cfg.seq, "gemm": frac(st, gemms),
+                     "attention": frac(st, ["attention"])}
+        del bw, blk, xi, xt, ws
+    # one sequence-parallel rank's share at 1280^2: attention over all 6912 tokens for 6 heads ...
+    cfg = si.CONFIGS["headslice_1280"]
+    B, S, H, hd = cfg.batch, cfg.seq, cfg.heads, cfg.head_dim
+    qkv = torch.randn((B, S, 3, H, hd), generator=g, device="cuda").to(torch.bfloat16)
+    o = torch.empty((B, S, H * hd), device="cuda", dtype=torch.bfloat16)
+    D = H * hd
+    flat = qkv.view(-1)
+    ms_a, st = timed(lambda: d.joint_attention(flat[0:], flat[D:], flat[2 * D:], o, B, H, S, hd,
+                                               (S * 3 * D, 3 * D, hd), (S * D, D, hd)))
+    # ... and the full-width MLP on its 1600 + 128 token slice
+    cm = si.CONFIGS["mlp_slice_1280"]
+    bw = {s: {t: w(shp) for t, shp in si.block_weight_shapes(cm).items()} for s in si.STREAMS}
+    blk = d.block_weights(bw["img"], bw["txt"])
+    c = d.block_config(cm.hidden, cm.heads, cm.head_dim, cm.mlp_hidden, cm.n_img, cm.n_txt, cm.grid_h, cm.grid_w,
+                       rope=cm.rope, dtype=cm.dtype)
+    temb = torch.randn((cm.batch, cm.hidden), generator=g, device="cuda")
+    xi = torch.randn((cm.batch, cm.n_img, cm.hidden), generator=g, device="cuda").to(torch.bfloat16)
+    xt = torch.randn((cm.batch, cm.n_txt, cm.hidden), generator=g, device="cuda").to(torch.bfloat16)
+    ws = d.workspace(d.dit_block_workspace_bytes(c, cm.batch))
+    ms_m, st_m = timed(lambda: d.dit_block_mlp(c, blk, temb, xi, xt, ws))
+    out["sp_rank_1280"] = {"attention_ms": round(ms_a, 3), "attention": frac(st, ["attention"]),
+                           "mlp_ms": round(ms_m, 3), "mlp_gemm": frac(st_m, ["gemm_mlp_up_gelu", "gemm_mlp_down_gate"]),
+                           "K": B, "heads": H, "tokens": S, "mlp_tokens": cm.seq}
+    return out
+
+
 def cpu_baseline(cfg, n_seeds):
     """Time the oracle on a bounded sample: one block for `n_seeds` seeds (all rows),
     scaled to a full step (blocks x K seeds). Block work dominates the step."""
@@ -365,7 +442,14 @@ def cpu_baseline(cfg, n_seeds):
     sec = time.perf_counter() - t0
     per_seed_block = sec / n_seeds
     ms_step = per_seed_block * cfg.blocks * cfg.batch * 1e3
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), "")
+    except OSError:
+        pass
     return {"value": round(ms_step, 1), "unit": "ms per K-seed denoise step", "cores": int(threads), "kind": "oracle",
+            "cpu_model": model,
             "sample": f"fp64 numpy oracle, one MMDiT block for {n_seeds} seed(s) at the step's shape "
                       f"({cfg.seq} tokens, hidden {cfg.hidden}), {sec:.1f} s measured, scaled x{cfg.blocks} blocks "
                       f"x{cfg.batch} seeds"}
@@ -437,6 +521,9 @@ def main():
                                  if summary["attention_tflops"] else None)
 
     extra = next_rows(torch, d, cfg, x)
+    del x, step
+    torch.cuda.empty_cache()
+    blocks = other_configs(torch, d) if args.config == "step_512_k16" else None
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -456,6 +543,7 @@ def main():
         "mfma_summary": summary,
         "kernels": kernels,
         "next_rows": extra,
+        "other_configs": blocks,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
