@@ -46,6 +46,9 @@ def parse():
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--config", default="step_512_k16", choices=[k for k, v in si.CONFIGS.items() if v.blocks >= 1])
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--headline-only", action="store_true",
+                   help="time only the denoise step (no next-row or other-configuration measurements), so that "
+                        "a profiler run sees only the step's kernels")
     p.add_argument("--cpu-sample-seeds", type=int, default=16)
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                    help="only run 5 plain device copies of MIB MiB (torch copy kernel); used to scale the "
@@ -135,7 +138,7 @@ def kernel_summary(run_dir, bench_json):
              "K=16 seeds,", "SDE flow update, reward statistics 64x16 (bf16 weights and activations, fp32 "
              "accumulation).", "", "Commands (repo root, on one MI355X):", "",
              f"    rocprofv3 --kernel-trace --stats --output-format csv -d {run_dir} -o bench -- python3 bench.py "
-             "--steps 5 --warmup 2 --no-cpu-baseline",
+             "--steps 5 --warmup 2 --no-cpu-baseline --headline-only",
              f"    python3 bench.py --kernel-summary {run_dir}", "",
              "The trace covers the bench's setup (torch kernels that draw the synthetic weights) plus 5 + 2 "
              "timed/warm-up steps", "and one event-instrumented step (8 steps in all). Library kernels, sorted "
@@ -213,7 +216,8 @@ def traffic_summary(run_dir, cfg):
                                bytes_per_launch=copy_bytes, fetch_scale=round(scale["FETCH_SIZE"], 5),
                                write_scale=round(scale["WRITE_SIZE"], 5)),
            "commands": [f"rocprofv3 --pmc {c} --output-format csv -d {run_dir}/{k}_{c} -o {k[0]} -- python3 bench.py "
-                        + ("--copy-calibration 1024" if k == "calib" else "--steps 1 --warmup 1 --no-cpu-baseline")
+                        + ("--copy-calibration 1024" if k == "calib"
+                           else "--steps 1 --warmup 1 --no-cpu-baseline --headline-only")
                         for k in ("calib", "bench") for c in ("FETCH_SIZE", "WRITE_SIZE")]
                        + [f"python3 bench.py --traffic-summary {run_dir}"],
            "per_kernel_class": classes}
@@ -520,10 +524,12 @@ def main():
     summary["attention_frac"] = (round(summary["attention_tflops"] / PEAK_BF16_TFLOPS, 4)
                                  if summary["attention_tflops"] else None)
 
-    extra = next_rows(torch, d, cfg, x)
-    del x, step
-    torch.cuda.empty_cache()
-    blocks = other_configs(torch, d) if args.config == "step_512_k16" else None
+    extra = blocks = None
+    if not args.headline_only:
+        extra = next_rows(torch, d, cfg, x)
+        del x, step
+        torch.cuda.empty_cache()
+        blocks = other_configs(torch, d) if args.config == "step_512_k16" else None
 
     cpu = None
     if not args.no_cpu_baseline:
