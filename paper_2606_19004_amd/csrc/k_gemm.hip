@@ -100,6 +100,17 @@ __device__ __forceinline__ void epilogue4(const GemmProblem& P, const RowEpi& R,
 // bf16 MFMA GEMM
 // ---------------------------------------------------------------------------
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
+typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+
+// Direct-to-LDS 16-byte-per-lane buffer load (M0 = LDS destination of lane 0), written as inline
+// assembly so that the compiler does not track it: with LDS addresses chosen at run time it cannot
+// prove that a later LDS read does not alias the load, and would wait for all loads in flight. The
+// caller's explicit s_waitcnt vmcnt is the only synchronisation for these loads. rsrc is a raw
+// buffer descriptor (base, stride 0, num_records, flags).
+__device__ __forceinline__ void dma_b128(u32x4_t rsrc, uint32_t m0v, uint32_t voff, uint32_t soff) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+               : : "s"(m0v), "v"(voff), "s"(rsrc), "s"(soff) : "memory", "m0");
+}
 
 __device__ __forceinline__ void tile_coords(int tl, int mt, int nt, int& tm, int& tn) {
   constexpr int GROUP_M = 8;
@@ -156,7 +167,9 @@ template <> struct Mfma<16> {
 
 // MS = MFMA block size (32 or 16); under sustained load with random operands the 16x16x32
 // form delivers more MFMA throughput per watt on this chip.
-template <int BM, int BN, int WM, int WN, int EPI, bool OUTF32, int MS = 32>
+// TRI (256 x 256 tiles only): three LDS stages for A and two for W (160 KB), so the activation
+// operand is loaded two k-tiles ahead; used when K is long and A streams from HBM.
+template <int BM, int BN, int WM, int WN, int EPI, bool OUTF32, int MS = 32, bool TRI = false>
 __global__ void __launch_bounds__(WM * WN * 64) gemm_bf16_kernel(GemmPair pr, int tiles0, int total_tiles) {
   typedef typename Mfma<MS>::acc_t acc_t;
   constexpr int NACC = sizeof(acc_t) / 4;              // accumulator registers per block
@@ -168,6 +181,7 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_bf16_kernel(GemmPair pr, in
   constexpr int A_LOADS = BM / 8 / NW, W_LOADS = BN / 8 / NW;  // 8-row groups each wave loads per k-tile
   constexpr int A_BYTES = BM * BK * 2, W_BYTES = BN * BK * 2;
   static_assert(A_LOADS >= 1 && W_LOADS >= 1, "every wave loads at least one row group");
+  static_assert(!TRI || (BM == 256 && BN == 256), "three A stages only for the 256 x 256 tile");
 #if defined(__HIP_DEVICE_COMPILE__)  // the buffer-resource builtins exist only in the device pass
   extern __shared__ __attribute__((aligned(1024))) char smem[];
 
@@ -207,6 +221,26 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_bf16_kernel(GemmPair pr, in
     int n = n0 + 8 * g + lrow;
     woff[i] = n < P.N ? (uint32_t)((int64_t)n * K * 2 + chunk * 16) : OOB;
   }
+  // TRI layout: [W0][W1][A0][A1][A2]; tile kt uses W stage kt % 2 and A stage kt % 3
+  auto stage_w = [&](int kt) -> char* { return smem + (kt & 1) * W_BYTES; };
+  auto stage_a = [&](int kt) -> char* { return smem + 2 * W_BYTES + (kt % 3) * A_BYTES; };
+  const int wave_s = __builtin_amdgcn_readfirstlane(wave);
+  const uint64_t pa64 = (uint64_t)P.A, pw64 = (uint64_t)P.W;
+  const u32x4_t ra4 = {(uint32_t)pa64, (uint32_t)(pa64 >> 32) & 0xffffu, 0x7fffffffu, 0x00020000u};
+  const u32x4_t rw4 = {(uint32_t)pw64, (uint32_t)(pw64 >> 32) & 0xffffu, 0x7fffffffu, 0x00020000u};
+  const uint32_t smem_lds = (uint32_t)(uintptr_t)(lds_ptr_t)smem;
+  auto issue_a = [&](int kt) {
+    const uint32_t sa = smem_lds + (uint32_t)(stage_a(kt) - smem);
+    const uint32_t soff = kt * BK * 2;
+#pragma unroll
+    for (int i = 0; i < A_LOADS; i++) dma_b128(ra4, sa + (wave_s * A_LOADS + i) * 1024, aoff[i], soff);
+  };
+  auto issue_w = [&](int kt) {
+    const uint32_t sw = smem_lds + (uint32_t)(stage_w(kt) - smem);
+    const uint32_t soff = kt * BK * 2;
+#pragma unroll
+    for (int i = 0; i < W_LOADS; i++) dma_b128(rw4, sw + (wave_s * W_LOADS + i) * 1024, woff[i], soff);
+  };
   auto issue = [&](int kt, int buf) {
     char* sa = smem + buf * (A_BYTES + W_BYTES);
     char* sw = sa + A_BYTES;
@@ -239,9 +273,9 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_bf16_kernel(GemmPair pr, in
   const int wrow0 = (wn * WTN + frow) * 128, arow0 = (wm * WTM + frow) * 128;
   // fragments of k step s, register-double-buffered so step s+1 loads while step s multiplies
   bf16x8 fw[2][TI], fa[2][TJ];
-  auto frags = [&](int buf, int s, int rb) {
-    const char* sa = smem + buf * (A_BYTES + W_BYTES);
-    const char* sw = sa + A_BYTES;
+  auto frags = [&](int buf, int s, int rb) {   // TRI: buf is the k-tile index
+    const char* sa = TRI ? stage_a(buf) : smem + buf * (A_BYTES + W_BYTES);
+    const char* sw = TRI ? stage_w(buf) : sa + A_BYTES;
     const int c = (KS / 8) * s + lkc;
 #pragma unroll
     for (int i = 0; i < TI; i++) fw[rb][i] = *(const bf16x8*)(sw + wrow0 + MS * i * 128 + ((c ^ fwk[i]) << 4));
@@ -284,14 +318,59 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_bf16_kernel(GemmPair pr, in
     }
   };
 
-  issue(0, 0);
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  if (nk > 1) issue(1, 1);
-  frags(0, 0, 0);
-  for (int kt = 0; kt + 2 < nk; kt++) ktile(kt, std::integral_constant<int, 0>());
-  if (nk >= 2) ktile(nk - 2, std::integral_constant<int, 1>());
-  ktile(nk - 1, std::integral_constant<int, 2>());
+  if constexpr (TRI) {
+    // k-tile kt, last step: wait for tile kt+1 (the A loads of tile kt+2, issued last, may still be
+    // in flight), barrier, then refill W stage kt % 2 with tile kt+2 and A stage kt % 3 with tile
+    // kt+3, and read tile kt+1's first fragments. Loads are issued W first, then A, so that
+    // vmcnt(A_LOADS) leaves exactly the newest A loads outstanding.
+    auto ktile3 = [&](int kt, auto ph_c) {
+      constexpr int PH = decltype(ph_c)::value;   // 0: W+A refill, 1: W refill, 2: none, 3: last tile
+#pragma unroll
+      for (int s = 0; s < BK / KS; s++) {
+        const int rb = s & 1;
+        const bool seam = s == BK / KS - 1;
+        if (!seam) {
+          frags(kt, s + 1, rb ^ 1);
+        } else if (PH < 3) {
+          if (PH < 2) __builtin_amdgcn_s_waitcnt(0x0070 | A_LOADS);   // vmcnt(A_LOADS) lgkmcnt(0)
+          else __builtin_amdgcn_s_waitcnt(0);
+          __syncthreads();
+          if (PH <= 1) issue_w(kt + 2);
+          if (PH == 0) issue_a(kt + 3);
+          frags(kt + 1, 0, rb ^ 1);
+        }
+#pragma unroll
+        for (int i = 0; i < TI; i++)
+#pragma unroll
+          for (int j = 0; j < TJ; j++)
+            acc[i][j] = Mfma<MS>::run(fw[rb][i], fa[rb][j], acc[i][j]);
+        if (!seam) sched_step<NM, 0, TI + TJ>();
+        else sched_step<NM, PH == 0 ? A_LOADS + W_LOADS : (PH == 1 ? W_LOADS : 0), PH < 3 ? TI + TJ : 0>();
+      }
+    };
+    issue_a(0);
+    issue_w(0);
+    if (nk > 1) issue_a(1);
+    if (nk > 1) __builtin_amdgcn_s_waitcnt(0x0070 | A_LOADS);
+    else __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (nk > 1) issue_w(1);
+    if (nk > 2) issue_a(2);
+    frags(0, 0, 0);
+    for (int kt = 0; kt + 3 < nk; kt++) ktile3(kt, std::integral_constant<int, 0>());
+    if (nk >= 3) ktile3(nk - 3, std::integral_constant<int, 1>());
+    if (nk >= 2) ktile3(nk - 2, std::integral_constant<int, 2>());
+    ktile3(nk - 1, std::integral_constant<int, 3>());
+  } else {
+    issue(0, 0);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (nk > 1) issue(1, 1);
+    frags(0, 0, 0);
+    for (int kt = 0; kt + 2 < nk; kt++) ktile(kt, std::integral_constant<int, 0>());
+    if (nk >= 2) ktile(nk - 2, std::integral_constant<int, 1>());
+    ktile(nk - 1, std::integral_constant<int, 2>());
+  }
 
   // ---- epilogue: bias, gate vectors and the RoPE table are staged in LDS once per tile ----
   constexpr int LDS_BYTES = 2 * (A_BYTES + W_BYTES);
@@ -320,6 +399,23 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_bf16_kernel(GemmPair pr, in
   //   MS = 32: n = 32 i + 8 g + 4 (lane / 32) + q, m = 32 j + lane % 32
   //   MS = 16: n = 16 i + 4 (lane / 16) + q,        m = 16 j + lane % 16
   constexpr int NG = NACC / 4;
+  // MS = 16: the residual values of this wave's whole sub-tile (one 4-column group per block (i, j),
+  // 64 registers, free now that the fragment registers are dead) are requested at once, so their
+  // memory latency is paid once per tile instead of once per block
+  constexpr bool XALL = EPI == EPI_RESID && MS == 16;
+  uint2 xall[XALL ? TJ : 1][XALL ? TI : 1];
+  if constexpr (XALL) {
+#pragma unroll
+    for (int j = 0; j < TJ; j++) {
+      const int m = m0 + wm * WTM + MS * j + frow;
+      const int64_t off = m < P.M ? row_epi(P, m).off : 0;
+#pragma unroll
+      for (int i = 0; i < TI; i++) {
+        const int n = n0 + wn * WTN + MS * i + 4 * lkc;
+        if (m < P.M && n < P.N) xall[j][i] = *(const uint2*)((const u16*)P.C + off + n);
+      }
+    }
+  }
 #pragma unroll
   for (int j = 0; j < TJ; j++) {
     int m = m0 + wm * WTM + MS * j + frow;
@@ -335,10 +431,10 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_bf16_kernel(GemmPair pr, in
         if (EPI == EPI_RESID && n < P.N) xr[slot][g] = *(const uint2*)((const u16*)P.C + R.off + n);
       }
     };
-    if (EPI == EPI_RESID) load_x(0, 0);
+    if (EPI == EPI_RESID && !XALL) load_x(0, 0);
 #pragma unroll
     for (int i = 0; i < TI; i++) {
-      if (EPI == EPI_RESID && i + 1 < TI) load_x(i + 1, (i + 1) & 1);
+      if (EPI == EPI_RESID && !XALL && i + 1 < TI) load_x(i + 1, (i + 1) & 1);
 #pragma unroll
       for (int g = 0; g < NG; g++) {
         int nl = wn * WTN + MS * i + 8 * g + 4 * lkc;   // column inside the tile
@@ -354,7 +450,7 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_bf16_kernel(GemmPair pr, in
         if (EPI == EPI_RESID) {
           float4 gv = gate_lds ? *(const float4*)(s_gate + bt * BN + nl)
                                : *(const float4*)(P.gate + R.gate + n);
-          uint2 u = xr[i & 1][g];
+          uint2 u = XALL ? xall[XALL ? j : 0][XALL ? i : 0] : xr[i & 1][g];
           v[0] = fmaf(gv.x, v[0], __uint_as_float(u.x << 16));
           v[1] = fmaf(gv.y, v[1], __uint_as_float(u.x & 0xffff0000u));
           v[2] = fmaf(gv.z, v[2], __uint_as_float(u.y << 16));
@@ -381,39 +477,42 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_bf16_kernel(GemmPair pr, in
 #endif
 }
 
-template <int BM, int BN, int WM, int WN, int EPI, bool OUTF32, int MS>
+template <int BM, int BN, int WM, int WN, int EPI, bool OUTF32, int MS, bool TRI = false>
 static hipError_t launch_bf16(const GemmPair& pr, hipStream_t s) {
   int tiles[2] = {0, 0};
   for (int i = 0; i < pr.nprob; i++)
     if (pr.p[i].M > 0 && pr.p[i].N > 0) tiles[i] = cdiv(pr.p[i].M, BM) * cdiv(pr.p[i].N, BN);
   int total = tiles[0] + tiles[1];
   if (total == 0) return hipSuccess;
-  size_t lds = 2 * (size_t)(BM + BN) * 64 * 2;
+  size_t lds = TRI ? (size_t)(2 * BN + 3 * BM) * 64 * 2 : 2 * (size_t)(BM + BN) * 64 * 2;
   static bool attr_set[64] = {};
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) dev = 0;
   if (lds > 65536 && dev < 64 && !attr_set[dev]) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_kernel<BM, BN, WM, WN, EPI, OUTF32, MS>),
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_kernel<BM, BN, WM, WN, EPI, OUTF32, MS, TRI>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     attr_set[dev] = true;
   }
   int grid = 8 * cdiv(total, 8);
-  gemm_bf16_kernel<BM, BN, WM, WN, EPI, OUTF32, MS><<<grid, WM * WN * 64, lds, s>>>(pr, tiles[0], total);
+  gemm_bf16_kernel<BM, BN, WM, WN, EPI, OUTF32, MS, TRI><<<grid, WM * WN * 64, lds, s>>>(pr, tiles[0], total);
   return hipGetLastError();
 }
 
 template <int EPI, bool OUTF32>
 static hipError_t dispatch_bf16(const GemmPair& pr, hipStream_t s) {
-  int maxn = 0;
+  int maxn = 0, mink = 1 << 30;
   int64_t big_tiles = 0;
   for (int i = 0; i < pr.nprob; i++) {
     maxn = std::max(maxn, pr.p[i].N);
+    if (pr.p[i].M > 0 && pr.p[i].N > 0) mink = std::min(mink, pr.p[i].K);
     big_tiles += (int64_t)cdiv(pr.p[i].M, 256) * cdiv(pr.p[i].N, 256);
   }
   if (maxn <= 64) return launch_bf16<64, 64, 2, 2, EPI, OUTF32, 32>(pr, s);
   if (big_tiles < 512) return launch_bf16<128, 128, 2, 2, EPI, OUTF32, 32>(pr, s);
   // large problems: 8 waves of 64x128 on 16x16x32 MFMAs (measured 3-7% faster than 32x32x16 here)
+  // long K (the MLP down projection): the activation rows stream from HBM, so they get a third stage
+  if (mink >= 8192) return launch_bf16<256, 256, 4, 2, EPI, OUTF32, 16, true>(pr, s);
   return launch_bf16<256, 256, 4, 2, EPI, OUTF32, 16>(pr, s);
 }
 

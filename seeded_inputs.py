@@ -97,6 +97,9 @@ CONFIGS = {
     # small bf16 cases for element-wise parity: several tiles plus ragged tails
     "small_bf16": Shape("small_bf16", 256, 2, 128, 7, 9, 21, 3),
     "small_bf16_d64": Shape("small_bf16_d64", 320, 5, 64, 11, 13, 37, 2),
+    # MLP half with a long down-projection (K = 4*2176 = 8704) and ragged rows and columns
+    # (63 + 21 tokens x 3 seeds; 2176 output features): the three-stage GEMM path with partial tiles
+    "mlp_long_k": Shape("mlp_long_k", 2176, 17, 128, 7, 9, 21, 3, rope=False),
     "small_step_bf16": Shape("small_step_bf16", 256, 2, 128, 8, 12, 24, 4, blocks=2,
                              noise_level=0.7, dt=0.05, reward_groups=5, reward_n=4, reward_k=2),
 }

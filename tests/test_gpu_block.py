@@ -115,6 +115,22 @@ def test_block_mlp_half(d):
             check(cfg, g[b], O.mlp_half(w64[s], m, x64[b]), x64[b])
 
 
+def test_block_mlp_long_k_ragged(d):
+    """MLP half whose down projection has K >= 8192 (three A stages in LDS) on partial tiles: 189 image
+    and 63 text rows, 2176 output columns; every row is compared."""
+    cfg = si.CONFIGS["mlp_long_k"]
+    assert cfg.mlp_hidden >= 8192 and cfg.hidden % 256 != 0
+    inp = si.block_inputs(cfg)
+    gi, gt, _ = run_block(d, cfg, inp, mlp_only=True)
+    w64 = weights_f64(inp["weights"], cfg.dtype)
+    temb = inp["temb"].astype(np.float64)
+    for s, g, x in (("img", gi, inp["x_img"]), ("txt", gt, inp["x_txt"])):
+        x64 = si.as_f64(x, cfg.dtype)
+        for b in range(cfg.batch):
+            m = {k: v[0] for k, v in O.modulation(temb[b:b + 1], w64[s]["mod_w"], w64[s]["mod_b"]).items()}
+            check(cfg, g[b], O.mlp_half(w64[s], m, x64[b]), x64[b])
+
+
 def test_block_errors_write_nothing(d):
     cfg = si.CONFIGS["small_bf16"]
     inp = si.block_inputs(cfg)
