@@ -158,8 +158,8 @@ def kernel_summary(run_dir, bench_json):
     lines += ["", f"bench.py (no profiler): {b['value']} ms per step; dominant kernel `{r['kernel']}` averaged "
               f"{r['avg_launch_us']} us per launch with HIP events ({r['achieved']} TFLOP/s, "
               f"{100 * r['frac']:.1f}% of {r['peak']}).",
-              "EPI codes in `gemm_bf16_kernel<BM, BN, WM, WN, EPI, OUTF32, MS>`: 0 plain store, 1 GELU (MLP up), "
-              "2 gated residual (output projection, MLP down), 3 QKV with 2D RoPE; MS is the MFMA block size."]
+              "EPI codes in `gemm_bf16_kernel<BM, BN, WM, WN, EPI, OUTF32, MS, TRI>`: 0 plain store, 1 GELU (MLP up), "
+              "2 gated residual (output projection, MLP down), 3 QKV with 2D RoPE; MS is the MFMA block size; TRI marks three LDS stages for the activation operand (long K)."]
     with open(os.path.join(ROOT, KERNEL_MD), "w") as f:
         f.write("\n".join(lines) + "\n")
     print("\n".join(lines))
