@@ -1,21 +1,27 @@
 // GEMMs of the MMDiT block on gfx950: C = epilogue(A W^T + bias), W stored [N][K].
 //
-// bf16 path: LDS-staged MFMA kernel (v_mfma_f32_32x32x16_bf16, fp32 accumulate).
-//   * Computed as C^T = W A^T: MFMA operand "A" = 32 rows of W, operand "B" =
-//     32 rows of A; both are K-contiguous, so every lane reads one 16-byte
-//     chunk per fragment (ds_read_b128). The accumulator gives each lane one
-//     token row m and runs of 4 consecutive output features n, which is what
-//     the epilogues need (RoPE pairs (2i, 2i+1) sit in one lane).
+// bf16 path: LDS-staged MFMA kernel with fp32 accumulation.
+//   * Computed as C^T = W A^T: MFMA operand "A" = rows of W, operand "B" = rows
+//     of A; both are K-contiguous, so every lane reads one 16-byte chunk per
+//     fragment (ds_read_b128). The accumulator gives each lane one token row m
+//     and runs of 4 consecutive output features n, which is what the epilogues
+//     need (RoPE pairs (2i, 2i+1) sit in one lane).
 //   * Tiles of A and W move HBM -> LDS with buffer_load ... lds (no VGPR
-//     staging), double-buffered. Out-of-range rows use an offset past the
-//     buffer's num_records, which the hardware turns into zeros.
+//     staging). Out-of-range rows use an offset past the buffer's num_records,
+//     which the hardware turns into zeros.
 //   * LDS rows are 64 bf16 = 8 chunks of 16 bytes; chunk c of row r is stored
 //     at slot c ^ ((r ^ r >> 3) & 7), so the 16 lanes of a ds_read_b128 cycle
 //     hit 16 different bank groups of the 64-bank LDS.
-//   * The large tile (256 x 256) runs 8 waves (2 per SIMD), each 64 rows x 128
-//     features; fragments of the next 16-deep k step load while the current
-//     step's MFMAs run, and a k-tile barrier sits at the last step so it
-//     overlaps MFMAs in flight.
+//   * The large tile (256 x 256 x 64, v_mfma_f32_16x16x32_bf16) runs 8 waves
+//     (2 per SIMD), each 64 rows x 128 features, and keeps three LDS stages of
+//     A and two of W (160 KB), so the activation rows are requested two k-tiles
+//     before use. Fragments of the next 32-deep k step load while the current
+//     step's MFMAs run; the k-tile barrier sits at the last step, whose
+//     fragments are already in registers. Smaller problems use 128 x 128 or
+//     64 x 64 tiles with v_mfma_f32_32x32x16_bf16 and two stages of each.
+//   * Epilogue: bias, gate vectors and the RoPE table are staged in LDS per
+//     tile; the gated residual reads of a wave's whole sub-tile are issued at
+//     once.
 //   * Workgroups are dispatched round-robin over the 8 XCDs; tile t is given
 //     to workgroup ids so that each XCD owns one contiguous range of tiles,
 //     ordered in groups of 8 M-tiles so concurrently running tiles share A and
@@ -105,11 +111,15 @@ typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
 // Direct-to-LDS 16-byte-per-lane buffer load (M0 = LDS destination of lane 0), written as inline
 // assembly so that the compiler does not track it: with LDS addresses chosen at run time it cannot
 // prove that a later LDS read does not alias the load, and would wait for all loads in flight. The
-// caller's explicit s_waitcnt vmcnt is the only synchronisation for these loads. rsrc is a raw
-// buffer descriptor (base, stride 0, num_records, flags).
+// caller's explicit s_waitcnt vmcnt is the only synchronisation for these loads. M0 is reserved by
+// the compiler, so the sequence saves it in a scratch SGPR and restores it after issuing the load
+// (the destination is taken from M0 when the load issues). rsrc is a raw buffer descriptor (base,
+// stride 0, num_records, flags).
 __device__ __forceinline__ void dma_b128(u32x4_t rsrc, uint32_t m0v, uint32_t voff, uint32_t soff) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
-               : : "s"(m0v), "v"(voff), "s"(rsrc), "s"(soff) : "memory", "m0");
+  uint32_t saved;
+  asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\tbuffer_load_dwordx4 %2, %3, %4 offen lds\n\t"
+               "s_mov_b32 m0, %0"
+               : "=&s"(saved) : "s"(m0v), "v"(voff), "s"(rsrc), "s"(soff) : "memory");
 }
 
 __device__ __forceinline__ void tile_coords(int tl, int mt, int nt, int& tm, int& tn) {
@@ -168,7 +178,7 @@ template <> struct Mfma<16> {
 // MS = MFMA block size (32 or 16); under sustained load with random operands the 16x16x32
 // form delivers more MFMA throughput per watt on this chip.
 // TRI (256 x 256 tiles only): three LDS stages for A and two for W (160 KB), so the activation
-// operand is loaded two k-tiles ahead; used when K is long and A streams from HBM.
+// operand is loaded two k-tiles ahead.
 template <int BM, int BN, int WM, int WN, int EPI, bool OUTF32, int MS = 32, bool TRI = false>
 __global__ void __launch_bounds__(WM * WN * 64) gemm_bf16_kernel(GemmPair pr, int tiles0, int total_tiles) {
   typedef typename Mfma<MS>::acc_t acc_t;
@@ -501,19 +511,18 @@ static hipError_t launch_bf16(const GemmPair& pr, hipStream_t s) {
 
 template <int EPI, bool OUTF32>
 static hipError_t dispatch_bf16(const GemmPair& pr, hipStream_t s) {
-  int maxn = 0, mink = 1 << 30;
+  int maxn = 0;
   int64_t big_tiles = 0;
   for (int i = 0; i < pr.nprob; i++) {
     maxn = std::max(maxn, pr.p[i].N);
-    if (pr.p[i].M > 0 && pr.p[i].N > 0) mink = std::min(mink, pr.p[i].K);
     big_tiles += (int64_t)cdiv(pr.p[i].M, 256) * cdiv(pr.p[i].N, 256);
   }
   if (maxn <= 64) return launch_bf16<64, 64, 2, 2, EPI, OUTF32, 32>(pr, s);
   if (big_tiles < 512) return launch_bf16<128, 128, 2, 2, EPI, OUTF32, 32>(pr, s);
   // large problems: 8 waves of 64x128 on 16x16x32 MFMAs (measured 3-7% faster than 32x32x16 here)
-  // long K (the MLP down projection): the activation rows stream from HBM, so they get a third stage
-  if (mink >= 8192) return launch_bf16<256, 256, 4, 2, EPI, OUTF32, 16, true>(pr, s);
-  return launch_bf16<256, 256, 4, 2, EPI, OUTF32, 16>(pr, s);
+  // large problems: three A stages, so the activation rows are requested two k-tiles ahead (in the
+  // denoise step every block's weights and most activation panels arrive cold from HBM)
+  return launch_bf16<256, 256, 4, 2, EPI, OUTF32, 16, true>(pr, s);
 }
 
 // ---------------------------------------------------------------------------
