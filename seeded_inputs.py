@@ -100,6 +100,11 @@ CONFIGS = {
     # MLP half with a long down-projection (K = 4*2176 = 8704) and ragged rows and columns
     # (63 + 21 tokens x 3 seeds; 2176 output features): the three-stage GEMM path with partial tiles
     "mlp_long_k": Shape("mlp_long_k", 2176, 17, 128, 7, 9, 21, 3, rope=False),
+    # MLP halves with short up projections (K = 128 and 192: two and three 64-deep k-tiles) over
+    # 16 x (64x64 + 100) rows, enough 256 x 256 tiles to take the large-tile GEMM path, with a
+    # partial last row tile in each stream
+    "mlp_short_k128": Shape("mlp_short_k128", 128, 1, 128, 64, 64, 100, 16, rope=False),
+    "mlp_short_k192": Shape("mlp_short_k192", 192, 3, 64, 64, 64, 100, 16, rope=False),
     "small_step_bf16": Shape("small_step_bf16", 256, 2, 128, 8, 12, 24, 4, blocks=2,
                              noise_level=0.7, dt=0.05, reward_groups=5, reward_n=4, reward_k=2),
 }

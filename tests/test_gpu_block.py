@@ -131,6 +131,25 @@ def test_block_mlp_long_k_ragged(d):
             check(cfg, g[b], O.mlp_half(w64[s], m, x64[b]), x64[b])
 
 
+@pytest.mark.parametrize("name", ["mlp_short_k128", "mlp_short_k192"])
+def test_block_mlp_short_k_large_tiles(d, name):
+    """MLP half whose up projection has only two or three k-tiles (K = 128, 192) on enough rows
+    (16 x 4196) for the 256 x 256 tile path, the text stream's 1600 rows ending in a partial row
+    tile: sampled rows of both streams against the oracle."""
+    cfg = si.CONFIGS[name]
+    inp = si.block_inputs(cfg)
+    gi, gt, _ = run_block(d, cfg, inp, mlp_only=True)
+    w64 = weights_f64(inp["weights"], cfg.dtype)
+    rng = np.random.default_rng(11)
+    for b in (0, cfg.batch - 1):
+        for s, g, x, n in (("img", gi, inp["x_img"], cfg.n_img), ("txt", gt, inp["x_txt"], cfg.n_txt)):
+            mm = O.modulation(inp["temb"][b:b + 1].astype(np.float64), w64[s]["mod_w"], w64[s]["mod_b"])
+            m = {k: v[0] for k, v in mm.items()}
+            rows = np.unique(np.r_[0, n - 1, rng.choice(n, 40, replace=False)])
+            x64 = si.as_f64(x[b], cfg.dtype)[rows]
+            check(cfg, g[b][rows], O.mlp_half(w64[s], m, x64), x64)
+
+
 def test_block_errors_write_nothing(d):
     cfg = si.CONFIGS["small_bf16"]
     inp = si.block_inputs(cfg)
