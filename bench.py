@@ -34,6 +34,7 @@ PEAK_BF16_TFLOPS = 2516.6      # MI355X dense bf16 MFMA (256 CUs x 2.4 GHz x 409
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 TRAFFIC_JSON = "profiles/gemm_step_512_k16_traffic.json"
 KERNEL_MD = "profiles/step_512_k16_kernel_stats.md"
+MFMA_MD = "profiles/mfma_step_512_k16_counters.md"
 # source file whose kernels each counted class runs (a summary is stale once that file changes)
 CLASS_SOURCE = {"gemm_qkv_rope": "k_gemm.hip", "gemm_out_gate": "k_gemm.hip", "gemm_mlp_up_gelu": "k_gemm.hip",
                 "gemm_mlp_down_gate": "k_gemm.hip", "attention": "k_attn.hip", "ln_modulate": "k_elementwise.hip"}
@@ -56,6 +57,9 @@ def parse():
     p.add_argument("--traffic-summary", metavar="DIR", default=None,
                    help="no GPU: turn the four rocprofv3 --pmc runs under DIR (calib_FETCH_SIZE, "
                         "calib_WRITE_SIZE, bench_FETCH_SIZE, bench_WRITE_SIZE) into " + TRAFFIC_JSON)
+    p.add_argument("--mfma-summary", metavar="DIR", default=None,
+                   help="no GPU: turn a rocprofv3 --pmc run of SQ_VALU_MFMA_BUSY_CYCLES, SQ_INSTS_VALU_MFMA_MOPS_BF16 "
+                        "and GRBM_GUI_ACTIVE under DIR into " + "profiles/mfma_step_512_k16_counters.md")
     p.add_argument("--kernel-summary", metavar="DIR", default=None,
                    help="no GPU: turn rocprofv3 --kernel-trace --stats output under DIR (bench_kernel_stats.csv, "
                         "bench_kernel_trace.csv) plus the bench JSON line in DIR/../bench.json into " + KERNEL_MD)
@@ -163,6 +167,67 @@ def kernel_summary(run_dir, bench_json):
     with open(os.path.join(ROOT, KERNEL_MD), "w") as f:
         f.write("\n".join(lines) + "\n")
     print("\n".join(lines))
+
+
+def mfma_summary(run_dir, cfg):
+    """Per kernel class of the denoise step, from one rocprofv3 --pmc pass: MFMA busy cycles per SIMD
+    over the GPU-active clocks (rocprof's MfmaUtil), the clock those active cycles imply over the
+    dispatch's duration, and the bf16 MFMA flops the hardware counted (SQ_INSTS_VALU_MFMA_MOPS_BF16
+    is in units of 512) against the algorithmic count."""
+    import csv
+    import glob
+    files = glob.glob(os.path.join(run_dir, "*counter_collection.csv"))
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {run_dir}")
+    disp = {}
+    with open(files[0]) as f:
+        for r in csv.DictReader(f):
+            d = disp.setdefault(int(r["Dispatch_Id"]), {"row": r})
+            d[r["Counter_Name"]] = d.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    order = [disp[k] for k in sorted(disp)]
+    simds, xcds = 1024, 8
+    M, D, F = cfg.batch * cfg.seq, cfg.hidden, cfg.mlp_hidden
+    S = cfg.seq
+    algo = {"gemm_qkv_rope": 2.0 * M * D * 3 * D, "gemm_out_gate": 2.0 * M * D * D,
+            "gemm_mlp_up_gelu": 2.0 * M * D * F, "gemm_mlp_down_gate": 2.0 * M * F * D,
+            "attention": 4.0 * cfg.batch * S * S * D}
+    per = {}
+    for d, cls in zip(order, classify_dispatches([d["row"] for d in order])):
+        if cls not in algo:
+            continue
+        r = d["row"]
+        ns = float(r["End_Timestamp"]) - float(r["Start_Timestamp"])
+        active = d["GRBM_GUI_ACTIVE"] / xcds          # per-XCD value, summed over the 8 XCDs by rocprofv3
+        per.setdefault(cls, []).append((ns, active, d["SQ_VALU_MFMA_BUSY_CYCLES"], d["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512))
+    lines = ["# MFMA counters per kernel class: full K=16 denoise step (step_512_k16)", "",
+             "Command (repo root, one MI355X):", "",
+             f"    rocprofv3 --pmc SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU_MFMA_MOPS_BF16 GRBM_GUI_ACTIVE --output-format csv "
+             f"-d {run_dir} -o b -- python3 bench.py --steps 1 --warmup 1 --no-cpu-baseline --headline-only",
+             f"    python3 bench.py --mfma-summary {run_dir}", "",
+             "Per dispatch: MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE per XCD x 1024 SIMDs) (rocprof's "
+             "MfmaUtil); clock = GRBM_GUI_ACTIVE per XCD / dispatch duration; counted flops = "
+             "SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512. Dispatch durations here are under counter collection.", "",
+             "| class | dispatches | avg us | clock GHz | MFMA busy | TFLOP/s | % of 2516.6 | counted / algorithmic flops |",
+             "|---|---|---|---|---|---|---|---|"]
+    out = {}
+    for cls in ("gemm_qkv_rope", "gemm_out_gate", "gemm_mlp_up_gelu", "gemm_mlp_down_gate", "attention"):
+        v = per.get(cls)
+        if not v:
+            continue
+        n = len(v)
+        ns = sum(x[0] for x in v) / n
+        ghz = sum(x[1] / x[0] for x in v) / n
+        busy = sum(x[2] / (x[1] * simds) for x in v) / n
+        counted = sum(x[3] for x in v) / n
+        tf = algo[cls] / ns / 1e3
+        out[cls] = {"clock_ghz": round(ghz, 3), "mfma_busy": round(busy, 4), "counted_over_algorithmic": round(counted / algo[cls], 4)}
+        lines.append(f"| {cls} | {n} | {ns / 1e3:.1f} | {ghz:.2f} | {100 * busy:.1f}% | {tf:.0f} | "
+                     f"{100 * tf / PEAK_BF16_TFLOPS:.1f}% | {counted / algo[cls]:.4f} |")
+    lines += ["", "MFMA busy is measured against the clock the kernel actually ran at; the % column is against the "
+              "published peak, which assumes 2.4 GHz."]
+    with open(os.path.join(ROOT, MFMA_MD), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print(json.dumps(out))
 
 
 def traffic_summary(run_dir, cfg):
@@ -461,6 +526,9 @@ def cpu_baseline(cfg, n_seeds):
 
 def main():
     args = parse()
+    if args.mfma_summary:
+        mfma_summary(args.mfma_summary, si.CONFIGS[args.config])
+        return
     if args.traffic_summary:
         traffic_summary(args.traffic_summary, si.CONFIGS[args.config])
         return
