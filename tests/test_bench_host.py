@@ -1,5 +1,5 @@
 """Host-side logic of bench.py: classification of profiled dispatches into kernel classes and
-the staleness check of the committed traffic summary (no GPU)."""
+the staleness check of the committed traffic summary, and the MFMA counter summary (no GPU)."""
 import json
 
 import bench
@@ -33,3 +33,39 @@ def test_traffic_lookup_rejects_stale_source(tmp_path, monkeypatch):
     p.write_text(json.dumps(rec))
     assert bench.traffic_from_profile("gemm_mlp_down_gate") == 123
     assert bench.traffic_from_profile("attention") is None
+
+
+def test_mfma_summary_groups_counter_rows_by_dispatch(tmp_path, monkeypatch):
+    """Three counter rows per dispatch must classify as one dispatch (the out-projection / MLP-down
+    alternation counts dispatches), and the derived clock, MFMA-busy fraction and counted-flop ratio
+    follow from the counter definitions."""
+    import csv
+
+    import seeded_inputs as si
+    cfg = si.CONFIGS["step_512_k16"]
+    M, D, F = cfg.batch * cfg.seq, cfg.hidden, cfg.mlp_hidden
+    g = "void dit::gemm_bf16_kernel<256, 256, 4, 2, {}, false, 16, true>(dit::GemmPair, int, int)"
+    block = [(g.format(3), 2.0 * M * D * 3 * D), (g.format(2), 2.0 * M * D * D), (g.format(1), 2.0 * M * D * F),
+             (g.format(2), 2.0 * M * F * D)]
+    fields = ["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value", "Start_Timestamp", "End_Timestamp"]
+    rows, did = [], 0
+    for name, flops in block * 2:
+        did += 1
+        ns = 1.0e6                                   # 1 ms per dispatch
+        active = 2.0e6 * 8                           # 2 GHz on each of 8 XCDs
+        busy = 0.5 * 2.0e6 * 1024                    # half of the SIMD cycles
+        for c, v in (("GRBM_GUI_ACTIVE", active), ("SQ_VALU_MFMA_BUSY_CYCLES", busy),
+                     ("SQ_INSTS_VALU_MFMA_MOPS_BF16", flops / 512)):
+            rows.append({"Dispatch_Id": did, "Kernel_Name": name, "Counter_Name": c, "Counter_Value": v,
+                         "Start_Timestamp": 1000, "End_Timestamp": 1000 + ns})
+    with open(tmp_path / "b_counter_collection.csv", "w", newline="") as f:
+        w = csv.DictWriter(f, fieldnames=fields)
+        w.writeheader()
+        w.writerows(rows)
+    monkeypatch.setattr(bench, "MFMA_MD", str(tmp_path / "out.md"))
+    bench.mfma_summary(str(tmp_path), cfg)
+    text = (tmp_path / "out.md").read_text()
+    for cls in ("gemm_qkv_rope", "gemm_out_gate", "gemm_mlp_up_gelu", "gemm_mlp_down_gate"):
+        line = next(l for l in text.splitlines() if l.startswith(f"| {cls} |"))
+        cells = [c.strip() for c in line.strip("|").split("|")]
+        assert cells[1] == "2" and cells[3] == "2.00" and cells[4] == "50.0%" and cells[7] == "1.0000", line
