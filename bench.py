@@ -35,6 +35,9 @@ PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 TRAFFIC_JSON = "profiles/gemm_step_512_k16_traffic.json"
 KERNEL_MD = "profiles/step_512_k16_kernel_stats.md"
 MFMA_MD = "profiles/mfma_step_512_k16_counters.md"
+STALL_MD = "profiles/stalls_step_512_k16_counters.md"
+STALL_COUNTERS = ("SQ_WAVE_CYCLES", "SQ_WAIT_ANY", "SQ_WAIT_INST_ANY", "SQ_WAIT_INST_LDS", "SQ_ACTIVE_INST_ANY",
+                  "SQ_ACTIVE_INST_LDS", "SQ_LDS_BANK_CONFLICT", "SQ_INST_CYCLES_VMEM_RD", "GRBM_GUI_ACTIVE")
 # source file whose kernels each counted class runs (a summary is stale once that file changes)
 CLASS_SOURCE = {"gemm_qkv_rope": "k_gemm.hip", "gemm_out_gate": "k_gemm.hip", "gemm_mlp_up_gelu": "k_gemm.hip",
                 "gemm_mlp_down_gate": "k_gemm.hip", "attention": "k_attn.hip", "ln_modulate": "k_elementwise.hip"}
@@ -60,6 +63,10 @@ def parse():
     p.add_argument("--mfma-summary", metavar="DIR", default=None,
                    help="no GPU: turn a rocprofv3 --pmc run of SQ_VALU_MFMA_BUSY_CYCLES, SQ_INSTS_VALU_MFMA_MOPS_BF16 "
                         "and GRBM_GUI_ACTIVE under DIR into " + "profiles/mfma_step_512_k16_counters.md")
+    p.add_argument("--stall-summary", metavar="DIR", default=None,
+                   help="no GPU: turn a rocprofv3 --pmc run of the wave-state counters (SQ_WAVE_CYCLES, SQ_WAIT_ANY, "
+                        "SQ_WAIT_INST_ANY, SQ_WAIT_INST_LDS, SQ_ACTIVE_INST_ANY, SQ_ACTIVE_INST_LDS, SQ_LDS_BANK_CONFLICT, "
+                        "SQ_INST_CYCLES_VMEM_RD, GRBM_GUI_ACTIVE) under DIR into " + "profiles/stalls_step_512_k16_counters.md")
     p.add_argument("--kernel-summary", metavar="DIR", default=None,
                    help="no GPU: turn rocprofv3 --kernel-trace --stats output under DIR (bench_kernel_stats.csv, "
                         "bench_kernel_trace.csv) plus the bench JSON line in DIR/../bench.json into " + KERNEL_MD)
@@ -226,6 +233,62 @@ def mfma_summary(run_dir, cfg):
     lines += ["", "MFMA busy is measured against the clock the kernel actually ran at; the % column is against the "
               "published peak, which assumes 2.4 GHz."]
     with open(os.path.join(ROOT, MFMA_MD), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print(json.dumps(out))
+
+
+def _dispatch_counters(run_dir):
+    """Counter rows of one rocprofv3 --pmc run grouped per dispatch, in dispatch order, with the class of each."""
+    import csv
+    import glob
+    files = glob.glob(os.path.join(run_dir, "*counter_collection.csv"))
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {run_dir}")
+    disp = {}
+    with open(files[0]) as f:
+        for r in csv.DictReader(f):
+            d = disp.setdefault(int(r["Dispatch_Id"]), {"row": r})
+            d[r["Counter_Name"]] = d.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    order = [disp[k] for k in sorted(disp)]
+    return list(zip(order, classify_dispatches([d["row"] for d in order])))
+
+
+def stall_summary(run_dir):
+    """Where the waves of each kernel class spend their cycles, from one rocprofv3 --pmc pass of the SQ
+    wave-state counters. SQ_WAVE_CYCLES, SQ_WAIT_*, SQ_ACTIVE_INST_* and SQ_INST_CYCLES_VMEM_RD are
+    wave-cycles in units of 4 cycles, summed over waves; ratios to SQ_WAVE_CYCLES are fractions of the
+    waves' resident time. SQ_LDS_BANK_CONFLICT is in cycles (per CU, summed); it is shown per CU per
+    GPU-active cycle (GRBM_GUI_ACTIVE is summed over the 8 XCDs)."""
+    per = {}
+    for d, cls in _dispatch_counters(run_dir):
+        if cls:
+            per.setdefault(cls, []).append(d)
+    names = ["gemm_qkv_rope", "gemm_out_gate", "gemm_mlp_up_gelu", "gemm_mlp_down_gate", "attention", "ln_modulate"]
+    lines = ["# Wave-state counters per kernel class: full K=16 denoise step (step_512_k16)", "",
+             "Command (repo root, one MI355X):", "",
+             "    rocprofv3 --pmc " + " ".join(STALL_COUNTERS) + f" --output-format csv -d {run_dir} -o b -- "
+             "python3 bench.py --steps 1 --warmup 1 --no-cpu-baseline --headline-only",
+             f"    python3 bench.py --stall-summary {run_dir}", "",
+             "Fractions of the waves' resident cycles (SQ_WAVE_CYCLES): waiting for anything (SQ_WAIT_ANY), waiting "
+             "for an instruction to issue (SQ_WAIT_INST_ANY, of which LDS: SQ_WAIT_INST_LDS), executing any "
+             "instruction (SQ_ACTIVE_INST_ANY), executing LDS instructions (SQ_ACTIVE_INST_LDS), sending VMEM read "
+             "addresses (SQ_INST_CYCLES_VMEM_RD). LDS bank-conflict cycles are per CU per GPU-active cycle.", "",
+             "| class | dispatches | wait any | wait issue | wait LDS issue | active any | active LDS | VMEM rd issue | "
+             "LDS conflict / cycle |", "|---|---|---|---|---|---|---|---|---|"]
+    out = {}
+    for cls in names:
+        v = per.get(cls)
+        if not v:
+            continue
+        tot = {c: sum(d.get(c, 0.0) for d in v) for c in STALL_COUNTERS}
+        wc = tot["SQ_WAVE_CYCLES"] or 1.0
+        fr = {c: tot[c] / wc for c in ("SQ_WAIT_ANY", "SQ_WAIT_INST_ANY", "SQ_WAIT_INST_LDS", "SQ_ACTIVE_INST_ANY",
+                                        "SQ_ACTIVE_INST_LDS", "SQ_INST_CYCLES_VMEM_RD")}
+        conf = tot["SQ_LDS_BANK_CONFLICT"] / 256.0 / max(tot["GRBM_GUI_ACTIVE"] / 8.0, 1.0)
+        out[cls] = {k: round(x, 4) for k, x in fr.items()}
+        out[cls]["lds_conflict_per_cycle"] = round(conf, 4)
+        lines.append(f"| {cls} | {len(v)} | " + " | ".join(f"{100 * fr[c]:.1f}%" for c in fr) + f" | {conf:.4f} |")
+    with open(os.path.join(ROOT, STALL_MD), "w") as f:
         f.write("\n".join(lines) + "\n")
     print(json.dumps(out))
 
@@ -526,6 +589,9 @@ def cpu_baseline(cfg, n_seeds):
 
 def main():
     args = parse()
+    if args.stall_summary:
+        stall_summary(args.stall_summary)
+        return
     if args.mfma_summary:
         mfma_summary(args.mfma_summary, si.CONFIGS[args.config])
         return

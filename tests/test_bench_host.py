@@ -69,3 +69,42 @@ def test_mfma_summary_groups_counter_rows_by_dispatch(tmp_path, monkeypatch):
         line = next(l for l in text.splitlines() if l.startswith(f"| {cls} |"))
         cells = [c.strip() for c in line.strip("|").split("|")]
         assert cells[1] == "2" and cells[3] == "2.00" and cells[4] == "50.0%" and cells[7] == "1.0000", line
+
+
+def test_stall_summary_fractions_and_conflict_normalisation(tmp_path, monkeypatch):
+    """Wave-state counters are summed per kernel class and divided by SQ_WAVE_CYCLES; the LDS
+    bank-conflict count is normalised per CU (256) and per XCD-summed active cycle (8 XCDs)."""
+    import csv
+    g = "void dit::gemm_bf16_kernel<256, 256, 4, 2, {}, false, 16, true>(dit::GemmPair, int, int)"
+    ln = "void dit::ln_modulate_kernel<unsigned short, 6>(dit::LnArgs)"
+    block = [ln, g.format(3), "void dit::attn_fwd_bf16<128>(dit::AttnArgs)", g.format(2), ln, g.format(1), g.format(2)]
+    vals = {"SQ_WAVE_CYCLES": 1000.0, "SQ_WAIT_ANY": 300.0, "SQ_WAIT_INST_ANY": 400.0, "SQ_WAIT_INST_LDS": 25.0,
+            "SQ_ACTIVE_INST_ANY": 250.0, "SQ_ACTIVE_INST_LDS": 30.0, "SQ_INST_CYCLES_VMEM_RD": 20.0,
+            "SQ_LDS_BANK_CONFLICT": 256.0 * 100.0, "GRBM_GUI_ACTIVE": 8.0 * 1000.0}
+    assert set(vals) == set(bench.STALL_COUNTERS)
+    fields = ["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value", "Start_Timestamp", "End_Timestamp"]
+    rows, did = [], 0
+    for name in block * 2:
+        did += 1
+        for c, v in vals.items():
+            # the MLP-up class reads its wave cycles split over two rows of one dispatch
+            if name == g.format(1) and c == "SQ_WAVE_CYCLES":
+                rows += [{"Dispatch_Id": did, "Kernel_Name": name, "Counter_Name": c, "Counter_Value": v / 2,
+                          "Start_Timestamp": 0, "End_Timestamp": 1}] * 2
+                continue
+            rows.append({"Dispatch_Id": did, "Kernel_Name": name, "Counter_Name": c, "Counter_Value": v,
+                         "Start_Timestamp": 0, "End_Timestamp": 1})
+    with open(tmp_path / "b_counter_collection.csv", "w", newline="") as f:
+        w = csv.DictWriter(f, fieldnames=fields)
+        w.writeheader()
+        w.writerows(rows)
+    monkeypatch.setattr(bench, "STALL_MD", str(tmp_path / "out.md"))
+    bench.stall_summary(str(tmp_path))
+    text = (tmp_path / "out.md").read_text()
+    for cls, n in (("gemm_qkv_rope", 2), ("gemm_out_gate", 2), ("gemm_mlp_up_gelu", 2), ("gemm_mlp_down_gate", 2),
+                   ("attention", 2), ("ln_modulate", 4)):
+        line = next(l for l in text.splitlines() if l.startswith(f"| {cls} |"))
+        cells = [c.strip() for c in line.strip("|").split("|")]
+        assert cells[1] == str(n), line
+        assert cells[2:8] == ["30.0%", "40.0%", "2.5%", "25.0%", "3.0%", "2.0%"], line
+        assert cells[8] == "0.1000", line
