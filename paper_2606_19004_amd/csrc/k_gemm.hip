@@ -10,15 +10,19 @@
 //     staging). Out-of-range rows use an offset past the buffer's num_records,
 //     which the hardware turns into zeros.
 //   * LDS rows are 64 bf16 = 8 chunks of 16 bytes; chunk c of row r is stored
-//     at slot c ^ ((r ^ r >> 3) & 7), so the 16 lanes of a ds_read_b128 cycle
-//     hit 16 different bank groups of the 64-bank LDS.
+//     at slot c ^ ((r >> 1) & 7), so every lane group that a ds_read_b128 of a
+//     fragment is served in hits 16 different bank groups of the 64-bank LDS.
 //   * The large tile (256 x 256 x 64, v_mfma_f32_16x16x32_bf16) runs 8 waves
 //     (2 per SIMD), each 64 rows x 128 features, and keeps three LDS stages of
 //     A and two of W (160 KB), so the activation rows are requested two k-tiles
 //     before use. Fragments of the next 32-deep k step load while the current
 //     step's MFMAs run; the k-tile barrier sits at the last step, whose
-//     fragments are already in registers. Smaller problems use 128 x 128 or
-//     64 x 64 tiles with v_mfma_f32_32x32x16_bf16 and two stages of each.
+//     fragments are already in registers. The refill is split between the two
+//     steps of a k-tile (W after the barrier, A in the other step), and each
+//     wave lowers its issue priority as it advances between barriers, so the
+//     two waves of a SIMD share the matrix pipe instead of one running ahead
+//     and idling at the barrier. Smaller problems use 128 x 128 or 64 x 64
+//     tiles with v_mfma_f32_32x32x16_bf16 and two stages of each.
 //   * Epilogue: bias, gate vectors and the RoPE table are staged in LDS per
 //     tile; the gated residual reads of a wave's whole sub-tile are issued at
 //     once.
@@ -333,33 +337,47 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_bf16_kernel(GemmPair pr, in
   };
 
   if constexpr (TRI) {
-    // k-tile kt, last step: wait for tile kt+1 (the A loads of tile kt+2, issued last, may still be
-    // in flight), barrier, then refill W stage kt % 2 with tile kt+2 and A stage kt % 3 with tile
-    // kt+3, and read tile kt+1's first fragments. Loads are issued W first, then A, so that
-    // vmcnt(A_LOADS) leaves exactly the newest A loads outstanding.
+    // k-tile kt. First step: refill A stage (kt+2) % 3 with tile kt+2 (that stage last held tile
+    // kt-1, whose reads ended before the previous barrier). Last step: wait for tile kt+1 (the A
+    // loads of tile kt+2, issued last, may still be in flight: vmcnt(A_LOADS)), barrier, then
+    // refill W stage kt % 2 with tile kt+2 and read tile kt+1's first fragments.
+    // Issue priority between two barriers runs 3, 2 (halves of the last step), 1, 0 (halves of
+    // the next tile's first step): a wave that has run ahead yields the matrix pipe to the other
+    // wave of its SIMD, so both reach the barrier together.
     auto ktile3 = [&](int kt, auto ph_c) {
-      constexpr int PH = decltype(ph_c)::value;   // 0: W+A refill, 1: W refill, 2: none, 3: last tile
+      constexpr int PH = decltype(ph_c)::value;   // 0, 1: refill tile kt+2; 2: none; 3: last tile
 #pragma unroll
       for (int s = 0; s < BK / KS; s++) {
         const int rb = s & 1;
         const bool seam = s == BK / KS - 1;
         if (!seam) {
+          __builtin_amdgcn_s_setprio(1);
           frags(kt, s + 1, rb ^ 1);
+          if (PH <= 1) issue_a(kt + 2);
         } else if (PH < 3) {
           if (PH < 2) __builtin_amdgcn_s_waitcnt(0x0070 | A_LOADS);   // vmcnt(A_LOADS) lgkmcnt(0)
           else __builtin_amdgcn_s_waitcnt(0);
           __syncthreads();
+          __builtin_amdgcn_s_setprio(3);
           if (PH <= 1) issue_w(kt + 2);
-          if (PH == 0) issue_a(kt + 3);
           frags(kt + 1, 0, rb ^ 1);
         }
+        // the step's MFMAs in two halves; the priority drops between them (a scheduling boundary,
+        // so the step's reads and loads are placed among the first half's MFMAs)
 #pragma unroll
-        for (int i = 0; i < TI; i++)
+        for (int i = 0; i < TI / 2; i++)
 #pragma unroll
           for (int j = 0; j < TJ; j++)
             acc[i][j] = Mfma<MS>::run(fw[rb][i], fa[rb][j], acc[i][j]);
-        if (!seam) sched_step<NM, 0, TI + TJ>();
-        else sched_step<NM, PH == 0 ? A_LOADS + W_LOADS : (PH == 1 ? W_LOADS : 0), PH < 3 ? TI + TJ : 0>();
+        if (!seam) sched_step<NM / 2, PH <= 1 ? A_LOADS : 0, TI + TJ>();
+        else sched_step<NM / 2, PH <= 1 ? W_LOADS : 0, PH < 3 ? TI + TJ : 0>();
+        if (seam) __builtin_amdgcn_s_setprio(2);
+        else __builtin_amdgcn_s_setprio(0);
+#pragma unroll
+        for (int i = TI / 2; i < TI; i++)
+#pragma unroll
+          for (int j = 0; j < TJ; j++)
+            acc[i][j] = Mfma<MS>::run(fw[rb][i], fa[rb][j], acc[i][j]);
       }
     };
     issue_a(0);
@@ -369,12 +387,12 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_bf16_kernel(GemmPair pr, in
     else __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (nk > 1) issue_w(1);
-    if (nk > 2) issue_a(2);
     frags(0, 0, 0);
     for (int kt = 0; kt + 3 < nk; kt++) ktile3(kt, std::integral_constant<int, 0>());
     if (nk >= 3) ktile3(nk - 3, std::integral_constant<int, 1>());
     if (nk >= 2) ktile3(nk - 2, std::integral_constant<int, 2>());
     ktile3(nk - 1, std::integral_constant<int, 3>());
+    __builtin_amdgcn_s_setprio(0);
   } else {
     issue(0, 0);
     __builtin_amdgcn_s_waitcnt(0);
