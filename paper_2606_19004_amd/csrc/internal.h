@@ -38,12 +38,15 @@ template <> __device__ __forceinline__ void load4<float>(const float* p, float* 
   float4 a = *(const float4*)p;
   f[0] = a.x; f[1] = a.y; f[2] = a.z; f[3] = a.w;
 }
+// two fp32 values as packed bf16 (a in the low half), one v_cvt_pk_bf16_f32 (round to nearest even)
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, bf16x2_t));
+}
 template <typename T> __device__ __forceinline__ void store4(T* p, const float* f);
 template <> __device__ __forceinline__ void store4<u16>(u16* p, const float* f) {
-  uint2 u;
-  u.x = (uint32_t)from_f32<u16>(f[0]) | ((uint32_t)from_f32<u16>(f[1]) << 16);
-  u.y = (uint32_t)from_f32<u16>(f[2]) | ((uint32_t)from_f32<u16>(f[3]) << 16);
-  *(uint2*)p = u;
+  *(uint2*)p = make_uint2(pack_bf16x2(f[0], f[1]), pack_bf16x2(f[2], f[3]));
 }
 template <> __device__ __forceinline__ void store4<float>(float* p, const float* f) {
   *(float4*)p = make_float4(f[0], f[1], f[2], f[3]);

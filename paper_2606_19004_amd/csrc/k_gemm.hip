@@ -41,9 +41,11 @@ namespace dit {
 // epilogue on 4 consecutive output features n..n+3 of row m
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ float gelu_tanh_f(float z) {
-  // 0.5 z (1 + tanh(u)) = z * sigmoid(2u), u = sqrt(2/pi) (z + 0.044715 z^3)
-  float u2 = 2.0f * 0.7978845608028654f * fmaf(0.044715f * z, z * z, z);
-  return z * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-u2 * 1.4426950408889634f));
+  // 0.5 z (1 + tanh(u)) = z * sigmoid(2u), u = sqrt(2/pi) (z + 0.044715 z^3), and
+  // sigmoid(2u) = 1 / (1 + 2^(-2u log2 e)) with -2u log2 e = z (K1 + K2 z^2)
+  constexpr float K1 = -2.0f * 0.7978845608028654f * 1.4426950408889634f;
+  constexpr float K2 = K1 * 0.044715f;
+  return z * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(z * fmaf(K2, z * z, K1)));
 }
 
 
@@ -541,9 +543,9 @@ static hipError_t dispatch_bf16(const GemmPair& pr, hipStream_t s) {
   }
   if (maxn <= 64) return launch_bf16<64, 64, 2, 2, EPI, OUTF32, 32>(pr, s);
   if (big_tiles < 512) return launch_bf16<128, 128, 2, 2, EPI, OUTF32, 32>(pr, s);
-  // large problems: 8 waves of 64x128 on 16x16x32 MFMAs (measured 3-7% faster than 32x32x16 here)
-  // large problems: three A stages, so the activation rows are requested two k-tiles ahead (in the
-  // denoise step every block's weights and most activation panels arrive cold from HBM)
+  // large problems: 8 waves of 64x128 on 16x16x32 MFMAs (measured 3-7% faster than 32x32x16 here),
+  // with three A stages, so the activation rows are requested two k-tiles ahead (in the denoise step
+  // every block's weights and most activation panels arrive cold from HBM)
   return launch_bf16<256, 256, 4, 2, EPI, OUTF32, 16, true>(pr, s);
 }
 
