@@ -214,11 +214,34 @@ dit_status run_modulation(const dit_block_config* c, const dit_block_weights* w,
   return run_gemv(c, g, true, (float*)(ws + L.silu), ws + L.xs, "mod_gemv", s);
 }
 
-// h = LN(x)(1+scale)+shift for both streams into the joint [B][S][D] buffer
-dit_status run_ln(const dit_block_config* c, int B, const void* x_img, const void* x_txt, char* ws,
-                  const BlockWs& L, int shift_off, int scale_off, hipStream_t s) {
+// The modulation depends only on the timestep embedding, which every block of a step shares, so the
+// step computes it for up to MOD_GROUP blocks in one GEMV launch (2 weight slots per block):
+// dst + i * 2 B 6D holds block i's mod[s][b][6D], laid out as in run_modulation.
+constexpr int MOD_GROUP = GEMV_SLOTS / 2;
+dit_status run_modulation_group(const dit_block_config* c, const dit_block_weights* blocks, int n, int B,
+                                const float* temb, float* dst, char* ws, const BlockWs& L, hipStream_t s) {
   const int D = c->hidden;
-  float* mod = (float*)(ws + L.mod);
+  GemvArgs g{};
+  for (int i = 0; i < n; i++)
+    for (int st = 0; st < 2; st++) {
+      g.W[2 * i + st] = blocks[i].mod_w[st];
+      g.bias[2 * i + st] = blocks[i].mod_b[st];
+      g.out[2 * i + st] = dst + ((size_t)2 * i + st) * B * 6 * D;
+    }
+  g.out_bstride = 6 * D;
+  g.in = temb;
+  g.in_bstride = D;
+  g.N = 6 * D;
+  g.K = D;
+  g.B = B;
+  g.nstreams = 2 * n;
+  return run_gemv(c, g, true, (float*)(ws + L.silu), ws + L.xs, "mod_gemv", s);
+}
+
+// h = LN(x)(1+scale)+shift for both streams into the joint [B][S][D] buffer
+dit_status run_ln(const dit_block_config* c, int B, const void* x_img, const void* x_txt, const float* mod,
+                  char* ws, const BlockWs& L, int shift_off, int scale_off, hipStream_t s) {
+  const int D = c->hidden;
   LnArgs a{};
   a.x[0] = x_img;
   a.x[1] = x_txt;
@@ -256,13 +279,12 @@ GemmProblem problem(const void* A, RowMap am, const void* W, const void* bias, v
 
 // the MLP half: h2 = LN(x)(1+scale2)+shift2; u = GELU(W1 h2 + b1); x += gate2 (W2 u + b2)
 dit_status run_mlp_half(const dit_block_config* c, const dit_block_weights* w, int B, void* x_img, void* x_txt,
-                        char* ws, const BlockWs& L, hipStream_t s) {
+                        const float* mod, char* ws, const BlockWs& L, hipStream_t s) {
   const int D = c->hidden, F = c->mlp_hidden;
   const int rows[2] = {B * c->n_img, B * c->n_txt};
   void* x[2] = {x_img, x_txt};
   const int64_t nstream[2] = {c->n_img, c->n_txt};
-  float* mod = (float*)(ws + L.mod);
-  dit_status st = run_ln(c, B, x_img, x_txt, ws, L, 3 * D, 4 * D, s);
+  dit_status st = run_ln(c, B, x_img, x_txt, mod, ws, L, 3 * D, 4 * D, s);
   if (st) return st;
   GemmPair up{}, down{};
   up.nprob = down.nprob = 2;
@@ -280,7 +302,7 @@ dit_status run_mlp_half(const dit_block_config* c, const dit_block_weights* w, i
 }
 
 struct StepWs {
-  size_t temb, ximg, xtxt, v, inner, total;
+  size_t temb, ximg, xtxt, v, mods, inner, total;
 };
 
 size_t timestep_ws(const dit_block_config* c, int64_t B) {
@@ -302,6 +324,7 @@ StepWs step_layout(const dit_block_config* c, int64_t B, int C) {
   w.ximg = off; off += al256(B * c->n_img * c->hidden * es);
   w.xtxt = off; off += al256(B * c->n_txt * c->hidden * es);
   w.v = off;    off += al256(B * c->n_img * C * 4);
+  w.mods = off; off += al256((size_t)MOD_GROUP * 2 * B * 6 * c->hidden * 4);
   w.inner = off;
   size_t inner = std::max({block_layout(c, B).total, timestep_ws(c, B), patch_ws(c, B, C), final_ws(c, B)});
   w.total = off + inner;
@@ -455,26 +478,26 @@ size_t dit_block_workspace_bytes(const dit_block_config* cfg, int32_t batch) {
   return block_layout(cfg, batch).total;
 }
 
-dit_status dit_block_forward(const dit_block_config* c, const dit_block_weights* w, int32_t batch, const float* temb,
-                             void* x_img, void* x_txt, void* workspace, size_t workspace_bytes, dit_stream stream) {
-  dit_status st = check_block_args(c, w, batch, temb, x_img, x_txt);
-  if (st || batch == 0) return st;
-  BlockWs L = block_layout(c, batch);
-  if ((st = check_ws(workspace, workspace_bytes, L.total))) return st;
-  hipStream_t s = hs(stream);
-  char* ws = (char*)workspace;
-  const int B = batch, D = c->hidden, d = c->head_dim, H = c->heads;
+}  // extern "C"
+
+namespace {
+// One block on checked arguments. mod_pre: the block's modulation computed beforehand (layout of
+// run_modulation), or null to compute it here into the workspace.
+dit_status block_body(const dit_block_config* c, const dit_block_weights* w, int B, const float* temb, void* x_img,
+                      void* x_txt, char* ws, const BlockWs& L, const float* mod_pre, hipStream_t s) {
+  dit_status st = DIT_OK;
+  const int D = c->hidden, d = c->head_dim, H = c->heads;
   const int S = c->n_img + c->n_txt;
   const int rows[2] = {B * c->n_img, B * c->n_txt};
   void* x[2] = {x_img, x_txt};
   const int64_t nstream[2] = {c->n_img, c->n_txt};
-  float* mod = (float*)(ws + L.mod);
+  const float* mod = mod_pre ? mod_pre : (const float*)(ws + L.mod);
   float* rope = (float*)(ws + L.rope);
 
-  if ((st = run_modulation(c, w, B, temb, ws, L, s))) return st;
+  if (!mod_pre && (st = run_modulation(c, w, B, temb, ws, L, s))) return st;
   if (c->rope) TIMED("small_elementwise", 0, 0, s, rope_table(rope, std::max(c->grid_h, c->grid_w), d, c->rope_theta, s));
   // pre-attention LN + modulate into h
-  if ((st = run_ln(c, B, x_img, x_txt, ws, L, 0, D, s))) return st;
+  if ((st = run_ln(c, B, x_img, x_txt, mod, ws, L, 0, D, s))) return st;
   // QKV projection straight into the joint [B][S][3][H][d] buffer (+ RoPE on image q, k)
   GemmPair qkv{};
   qkv.nprob = 2;
@@ -520,7 +543,36 @@ dit_status dit_block_forward(const dit_block_config* c, const dit_block_weights*
     proj.p[i].gate_bstride = 6 * D;
   }
   TIMED("gemm_out_gate", gemm_flops(proj), 0, s, gemm(proj, EPI_RESID, c->dtype, false, s));
-  return run_mlp_half(c, w, B, x_img, x_txt, ws, L, s);
+  return run_mlp_half(c, w, B, x_img, x_txt, mod, ws, L, s);
+}
+
+// Blocks [0, n) in order on the block workspace `inner`; their modulation is computed MOD_GROUP
+// blocks at a time into mods (first_ready: the first group's is there already).
+dit_status run_blocks(const dit_block_config* c, const dit_block_weights* blocks, int n, int B, const float* temb,
+                      void* ximg, void* xtxt, float* mods, char* inner, const BlockWs& BL, bool first_ready,
+                      hipStream_t s) {
+  dit_status st = DIT_OK;
+  const size_t per = (size_t)2 * B * 6 * c->hidden;
+  for (int g0 = 0; g0 < n; g0 += MOD_GROUP) {
+    const int gn = std::min(MOD_GROUP, n - g0);
+    if (!(g0 == 0 && first_ready) && (st = run_modulation_group(c, blocks + g0, gn, B, temb, mods, inner, BL, s)))
+      return st;
+    for (int i = 0; i < gn; i++)
+      if ((st = block_body(c, &blocks[g0 + i], B, temb, ximg, xtxt, inner, BL, mods + i * per, s))) return st;
+  }
+  return DIT_OK;
+}
+}  // namespace
+
+extern "C" {
+
+dit_status dit_block_forward(const dit_block_config* c, const dit_block_weights* w, int32_t batch, const float* temb,
+                             void* x_img, void* x_txt, void* workspace, size_t workspace_bytes, dit_stream stream) {
+  dit_status st = check_block_args(c, w, batch, temb, x_img, x_txt);
+  if (st || batch == 0) return st;
+  BlockWs L = block_layout(c, batch);
+  if ((st = check_ws(workspace, workspace_bytes, L.total))) return st;
+  return block_body(c, w, batch, temb, x_img, x_txt, (char*)workspace, L, nullptr, hs(stream));
 }
 
 dit_status dit_block_mlp(const dit_block_config* c, const dit_block_weights* w, int32_t batch, const float* temb,
@@ -531,7 +583,7 @@ dit_status dit_block_mlp(const dit_block_config* c, const dit_block_weights* w, 
   if ((st = check_ws(workspace, workspace_bytes, L.total))) return st;
   char* ws = (char*)workspace;
   if ((st = run_modulation(c, w, batch, temb, ws, L, hs(stream)))) return st;
-  return run_mlp_half(c, w, batch, x_img, x_txt, ws, L, hs(stream));
+  return run_mlp_half(c, w, batch, x_img, x_txt, (const float*)(ws + L.mod), ws, L, hs(stream));
 }
 
 dit_status joint_attention(const void* q, const void* k, const void* v, void* o, int32_t batch, int32_t heads,
@@ -700,9 +752,10 @@ dit_status dit_denoise_step(const dit_block_config* c, const dit_step_weights* s
   if ((st = run_patch(c, sw, B, C, latent, ximg, inner, s))) return st;
   if (c->n_txt > 0)
     HIP_TRY(hipMemcpyAsync(xtxt, x_txt, (size_t)B * c->n_txt * c->hidden * esize(c->dtype), hipMemcpyDeviceToDevice, s));
-  size_t inner_bytes = workspace_bytes - L.inner;
-  for (int i = 0; i < n_blocks; i++)
-    if ((st = dit_block_forward(c, &blocks[i], B, temb, ximg, xtxt, inner, inner_bytes, stream))) return st;
+  const BlockWs BL = block_layout(c, B);
+  if (n_blocks > 0 && (st = check_ws(inner, workspace_bytes - L.inner, BL.total))) return st;
+  if ((st = run_blocks(c, blocks, n_blocks, B, temb, ximg, xtxt, (float*)(ws + L.mods), inner, BL, false, s)))
+    return st;
   if ((st = run_final(c, sw, B, C, temb, ximg, v, inner, s))) return st;
   TIMED("flow_step", 0, (noise_level > 0.f ? 16.0 : 12.0) * B * c->n_img * C, s,
         flow_update(latent, v, noise_level > 0.f ? noise : nullptr, (int64_t)B * c->n_img * C, cx, cv, ce, s));
@@ -812,12 +865,13 @@ dit_status dit_denoise_step_teacache(const dit_block_config* c, const dit_step_w
   if ((st = run_patch(c, sw, B, C, latent, ximg, inner, s))) return st;
   if (c->n_txt > 0)
     HIP_TRY(hipMemcpyAsync(xtxt, x_txt, (size_t)B * c->n_txt * D * esize(c->dtype), hipMemcpyDeviceToDevice, s));
-  // block 0's modulated input: its modulation GEMV and pre-attention LN (both streams; the
-  // image rows are compared), in the block workspace the first block will overwrite
+  // block 0's modulated input: the first group's modulation GEMV and block 0's pre-attention LN
+  // (both streams; the image rows are compared), in the block workspace the first block will overwrite
   const BlockWs BL = block_layout(c, B);
   if ((st = check_ws(inner, workspace_bytes - L.inner, BL.total))) return st;
-  if ((st = run_modulation(c, &blocks[0], B, temb, inner, BL, s))) return st;
-  if ((st = run_ln(c, B, ximg, xtxt, inner, BL, 0, D, s))) return st;
+  float* mods = (float*)(ws + L.mods);
+  if ((st = run_modulation_group(c, blocks, std::min(n_blocks, MOD_GROUP), B, temb, mods, inner, BL, s))) return st;
+  if ((st = run_ln(c, B, ximg, xtxt, mods, inner, BL, 0, D, s))) return st;
   const bool measure = state->has_prev != 0;
   TIMED("teacache_distance", 0, (measure ? 3.0 : 2.0) * n_act * esize(c->dtype), s,
         teacache_distance(inner + BL.h, cb + TL.hprev, B, c->n_img, c->n_txt, D, measure, parts, sums, c->dtype, s));
@@ -838,9 +892,7 @@ dit_status dit_denoise_step_teacache(const dit_block_config* c, const dit_step_w
   state->has_prev = 1;
   if (run) {
     TIMED("small_elementwise", 0, 0, s, teacache_residual(ximg, resid, n_act, 0, c->dtype, s));
-    size_t inner_bytes = workspace_bytes - L.inner;
-    for (int i = 0; i < n_blocks; i++)
-      if ((st = dit_block_forward(c, &blocks[i], B, temb, ximg, xtxt, inner, inner_bytes, stream))) return st;
+    if ((st = run_blocks(c, blocks, n_blocks, B, temb, ximg, xtxt, mods, inner, BL, true, s))) return st;
     TIMED("small_elementwise", 0, 0, s, teacache_residual(ximg, resid, n_act, 1, c->dtype, s));
     state->has_residual = 1;
   } else {

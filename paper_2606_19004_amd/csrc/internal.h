@@ -125,8 +125,11 @@ struct LnArgs {
 hipError_t ln_modulate(const LnArgs& a, int dtype, hipStream_t s);
 
 // out[s][b][n] = sum_k W[s][n][k] in[b][k] + bias[s][n]  (fp32 in/out, W in weight dtype)
+// up to GEMV_SLOTS independent weight matrices (same N, K, input) in one launch: the two streams of a
+// block, or the modulation of several blocks at once
+constexpr int GEMV_SLOTS = 16;
 struct GemvArgs {
-  const void* W[2]; const void* bias[2]; float* out[2];
+  const void* W[GEMV_SLOTS]; const void* bias[GEMV_SLOTS]; float* out[GEMV_SLOTS];
   int64_t out_bstride;
   const float* in; int64_t in_bstride;
   int N, K, B, nstreams;
