@@ -227,7 +227,8 @@ dit_status dit_final_layer(const dit_block_config* cfg, const dit_step_weights* 
                            int32_t latent_dim, const float* temb, const void* x_img, float* v,
                            void* workspace, size_t workspace_bytes, dit_stream stream);
 
-/* Workspace for dit_denoise_step (includes the residual streams). */
+/* Workspace for dit_denoise_step (includes the residual streams and the adaLN modulation of up to
+ * 8 blocks, which the step computes 8 blocks per GEMV launch). */
 size_t dit_denoise_workspace_bytes(const dit_block_config* cfg, int32_t batch, int32_t latent_dim);
 
 /* One K-seed denoise step: temb(t) -> patch embedding -> n_blocks blocks ->
