@@ -105,28 +105,49 @@ def traffic_from_profile(kernel_class):
 
 def classify_dispatches(rows):
     """Kernel class of every dispatch of one denoise-step run, in dispatch order. The two gated
-    residual GEMMs of a block share one kernel; the out-projection always precedes the MLP down."""
+    residual GEMMs of a block share one kernel; the out-projection always precedes the MLP down.
+    A GEMM call may be two launches (image rows on 256 x 256 tiles, then text rows on 256 x 192
+    tiles): the second launch takes the class of the first."""
     import re
     resid_seen = 0
     out = []
+    prev = None   # (EPI, class) of the previous dispatch when it was a 256 x 256 GEMM
     for r in rows:
         n = r["Kernel_Name"]
         m = re.search(r"gemm_bf16_kernel<(\d+), (\d+), (\d+), (\d+), (\d+)", n)
         cls = None
+        cur = None
         if m and int(m.group(1)) == 256:
-            epi = int(m.group(5))
-            if epi == 3:
+            epi, bn = int(m.group(5)), int(m.group(2))
+            if bn != 256 and prev is not None and prev[0] == epi:
+                cls = prev[1]
+            elif epi == 3:
                 cls = "gemm_qkv_rope"
             elif epi == 1:
                 cls = "gemm_mlp_up_gelu"
             elif epi == 2:
                 cls = "gemm_out_gate" if resid_seen % 2 == 0 else "gemm_mlp_down_gate"
                 resid_seen += 1
+            if bn == 256:
+                cur = (epi, cls)
         elif "attn_fwd" in n:
             cls = "attention"
         elif "ln_modulate_kernel" in n:
             cls = "ln_modulate"
+        prev = cur
         out.append(cls)
+    return out
+
+
+def group_calls(classes, values):
+    """Dispatches grouped into library calls: consecutive GEMM dispatches of one class are the image and
+    text launches of one call (no GEMM class follows itself otherwise). Returns (class, [values])."""
+    out = []
+    for cls, v in zip(classes, values):
+        if out and cls is not None and cls.startswith("gemm_") and out[-1][0] == cls:
+            out[-1][1].append(v)
+        else:
+            out.append((cls, [v]))
     return out
 
 
@@ -139,9 +160,10 @@ def kernel_summary(run_dir, bench_json):
     with open(os.path.join(run_dir, "bench_kernel_trace.csv")) as f:
         trace = sorted(csv.DictReader(f), key=lambda r: int(r["Start_Timestamp"]))
     per = {}
-    for r, cls in zip(trace, classify_dispatches(trace)):
+    durs = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-3 for r in trace]
+    for cls, v in group_calls(classify_dispatches(trace), durs):
         if cls:
-            per.setdefault(cls, []).append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-3)
+            per.setdefault(cls, []).append(sum(v))
     with open(bench_json) as f:
         b = json.loads([ln for ln in f if ln.startswith("{")][-1])
     lines = ["# Kernel time summary: full K=16 denoise step (step_512_k16)", "",
@@ -159,9 +181,10 @@ def kernel_summary(run_dir, bench_json):
         lines.append(f"| `{name}` | {r['Calls']} | {float(r['AverageNs']) * 1e-3:.2f} | "
                      f"{float(r['TotalDurationNs']) * 1e-6:.3f} |")
     lines += ["", "Per kernel class (classified per dispatch from the trace; `gemm_bf16_kernel<..., 2, ...>` runs "
-              "both the output projection and the MLP down, in that order within a block), against bench.py's "
+              "both the output projection and the MLP down, in that order within a block; a call's image and text "
+              "launches, where the text rows run on 256 x 192 tiles, are summed into one call), against bench.py's "
               "HIP-event average of the same class in a run without the profiler:", "",
-              "| class | dispatches | rocprofv3 avg us | bench.py events avg us |", "|---|---|---|---|"]
+              "| class | calls | rocprofv3 avg us per call | bench.py events avg us |", "|---|---|---|---|"]
     for cls, v in sorted(per.items(), key=lambda kv: -sum(kv[1])):
         ev = b.get("kernels", {}).get(cls, {}).get("avg_us")
         lines.append(f"| {cls} | {len(v)} | {sum(v) / len(v):.2f} | {ev if ev is not None else '-'} |")
@@ -199,22 +222,23 @@ def mfma_summary(run_dir, cfg):
             "gemm_mlp_up_gelu": 2.0 * M * D * F, "gemm_mlp_down_gate": 2.0 * M * F * D,
             "attention": 4.0 * cfg.batch * S * S * D}
     per = {}
-    for d, cls in zip(order, classify_dispatches([d["row"] for d in order])):
+    for cls, ds in group_calls(classify_dispatches([d["row"] for d in order]), order):
         if cls not in algo:
             continue
-        r = d["row"]
-        ns = float(r["End_Timestamp"]) - float(r["Start_Timestamp"])
-        active = d["GRBM_GUI_ACTIVE"] / xcds          # per-XCD value, summed over the 8 XCDs by rocprofv3
-        per.setdefault(cls, []).append((ns, active, d["SQ_VALU_MFMA_BUSY_CYCLES"], d["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512))
+        ns = sum(float(d["row"]["End_Timestamp"]) - float(d["row"]["Start_Timestamp"]) for d in ds)
+        active = sum(d["GRBM_GUI_ACTIVE"] for d in ds) / xcds   # per-XCD value, summed over the 8 XCDs by rocprofv3
+        per.setdefault(cls, []).append((ns, active, sum(d["SQ_VALU_MFMA_BUSY_CYCLES"] for d in ds),
+                                        sum(d["SQ_INSTS_VALU_MFMA_MOPS_BF16"] for d in ds) * 512))
     lines = ["# MFMA counters per kernel class: full K=16 denoise step (step_512_k16)", "",
              "Command (repo root, one MI355X):", "",
              f"    rocprofv3 --pmc SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU_MFMA_MOPS_BF16 GRBM_GUI_ACTIVE --output-format csv "
              f"-d {run_dir} -o b -- python3 bench.py --steps 1 --warmup 1 --no-cpu-baseline --headline-only",
              f"    python3 bench.py --mfma-summary {run_dir}", "",
-             "Per dispatch: MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE per XCD x 1024 SIMDs) (rocprof's "
-             "MfmaUtil); clock = GRBM_GUI_ACTIVE per XCD / dispatch duration; counted flops = "
-             "SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512. Dispatch durations here are under counter collection.", "",
-             "| class | dispatches | avg us | clock GHz | MFMA busy | TFLOP/s | % of 2516.6 | counted / algorithmic flops |",
+             "Per call (a GEMM call's image and text launches summed): MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / "
+             "(GRBM_GUI_ACTIVE per XCD x 1024 SIMDs) (rocprof's MfmaUtil); clock = GRBM_GUI_ACTIVE per XCD / dispatch "
+             "duration; counted flops = SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512. Dispatch durations here are under counter "
+             "collection.", "",
+             "| class | calls | avg us | clock GHz | MFMA busy | TFLOP/s | % of 2516.6 | counted / algorithmic flops |",
              "|---|---|---|---|---|---|---|---|"]
     out = {}
     for cls in ("gemm_qkv_rope", "gemm_out_gate", "gemm_mlp_up_gelu", "gemm_mlp_down_gate", "attention"):
@@ -317,9 +341,9 @@ def traffic_summary(run_dir, cfg):
     per = {}
     for c in ("FETCH_SIZE", "WRITE_SIZE"):
         rr = rows("bench_" + c)
-        for r, cls in zip(rr, classify_dispatches(rr)):
+        for cls, v in group_calls(classify_dispatches(rr), [float(r["Counter_Value"]) for r in rr]):
             if cls:
-                per.setdefault(cls, {}).setdefault(c, []).append(float(r["Counter_Value"]))
+                per.setdefault(cls, {}).setdefault(c, []).append(sum(v))
     M, D, F = cfg.batch * cfg.seq, cfg.hidden, cfg.mlp_hidden
     algo = {"gemm_qkv_rope": 2 * (M * D + 3 * D * D + 3 * M * D),
             "gemm_out_gate": 2 * (M * D + D * D + 2 * M * D),

@@ -201,7 +201,7 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_bf16_kernel(GemmPair pr, in
   constexpr int A_LOADS = BM / 8 / NW, W_LOADS = BN / 8 / NW;  // 8-row groups each wave loads per k-tile
   constexpr int A_BYTES = BM * BK * 2, W_BYTES = BN * BK * 2;
   static_assert(A_LOADS >= 1 && W_LOADS >= 1, "every wave loads at least one row group");
-  static_assert(!TRI || (BM == 256 && BN == 256), "three A stages only for the 256 x 256 tile");
+  static_assert(!TRI || (BM == 256 && (BN == 256 || BN == 192)), "three A stages only for 256-row tiles");
 #if defined(__HIP_DEVICE_COMPILE__)  // the buffer-resource builtins exist only in the device pass
   extern __shared__ __attribute__((aligned(1024))) char smem[];
 
@@ -533,6 +533,20 @@ static hipError_t launch_bf16(const GemmPair& pr, hipStream_t s) {
   return hipGetLastError();
 }
 
+// Compute units of the current device (one 256 x 256 workgroup fills a CU: 160 KB of LDS and the
+// whole register file), read once per device.
+static int cu_count() {
+  static int cus[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cus[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cus[dev] = n;
+  }
+  return cus[dev];
+}
+
 template <int EPI, bool OUTF32>
 static hipError_t dispatch_bf16(const GemmPair& pr, hipStream_t s) {
   int maxn = 0;
@@ -545,7 +559,32 @@ static hipError_t dispatch_bf16(const GemmPair& pr, hipStream_t s) {
   if (big_tiles < 512) return launch_bf16<128, 128, 2, 2, EPI, OUTF32, 32>(pr, s);
   // large problems: 8 waves of 64x128 on 16x16x32 MFMAs (measured 3-7% faster than 32x32x16 here),
   // with three A stages, so the activation rows are requested two k-tiles ahead (in the denoise step
-  // every block's weights and most activation panels arrive cold from HBM)
+  // every block's weights and most activation panels arrive cold from HBM).
+  //
+  // Every CU runs one 256 x 256 tile at a time, so a launch takes ceil(tiles / CUs) rounds of equal
+  // length. When the image and text problems together leave the last round partly empty, the text
+  // problem can instead run as a second launch of 256 x 192 tiles: with 4096 text rows and 3072 or
+  // 9216 output features that divides into whole rounds. A round of 256 x 192 tiles was measured at
+  // 0.80-0.83 of a 256 x 256 round (17% more operand bytes per flop than the 0.75 of the flops), so
+  // the split is taken when ceil(t_img / CUs) + 0.83 ceil(t_txt' / CUs) rounds beat
+  // ceil((t_img + t_txt) / CUs).
+  if (pr.nprob == 2 && pr.p[0].M > 0 && pr.p[1].M > 0 && pr.p[0].N > 0 && pr.p[1].N > 0) {
+    const int64_t cus = cu_count();
+    const int64_t t0 = (int64_t)cdiv(pr.p[0].M, 256) * cdiv(pr.p[0].N, 256);
+    const int64_t t1 = (int64_t)cdiv(pr.p[1].M, 256) * cdiv(pr.p[1].N, 256);
+    const int64_t t1n = (int64_t)cdiv(pr.p[1].M, 256) * cdiv(pr.p[1].N, 192);
+    const double merged = (double)((t0 + t1 + cus - 1) / cus);
+    const double split = (double)((t0 + cus - 1) / cus) + 0.83 * (double)((t1n + cus - 1) / cus);
+    if (split < merged) {
+      GemmPair a = pr, b = pr;
+      a.nprob = 1;
+      b.nprob = 1;
+      b.p[0] = pr.p[1];
+      hipError_t e = launch_bf16<256, 256, 4, 2, EPI, OUTF32, 16, true>(a, s);
+      if (e != hipSuccess) return e;
+      return launch_bf16<256, 192, 4, 2, EPI, OUTF32, 16, true>(b, s);
+    }
+  }
   return launch_bf16<256, 256, 4, 2, EPI, OUTF32, 16, true>(pr, s);
 }
 

@@ -23,6 +23,27 @@ def test_classify_dispatches_block_order():
     assert bench.classify_dispatches([_row("void dit::gemm_bf16_kernel<64, 64, 2, 2, 0, true, 32>(x)")]) == [None]
 
 
+def test_classify_dispatches_split_text_launch():
+    """A GEMM call whose text rows run as a second launch on 256 x 192 tiles: the second launch takes
+    the first one's class, the out-projection / MLP-down alternation still counts calls, and
+    group_calls sums the two launches into one call."""
+    g = "void dit::gemm_bf16_kernel<256, {}, 4, 2, {}, false, 16, true>(dit::GemmPair, int, int)"
+    ln = _row("void dit::ln_modulate_kernel<unsigned short, 6>(dit::LnArgs)")
+    block = [ln, _row(g.format(256, 3)), _row(g.format(192, 3)), _row("void dit::attn_fwd_bf16<128>(dit::AttnArgs)"),
+             _row(g.format(256, 2)), _row(g.format(192, 2)), ln, _row(g.format(256, 1)),
+             _row(g.format(256, 2)), _row(g.format(192, 2))]
+    got = bench.classify_dispatches(block * 2)
+    want = ["ln_modulate", "gemm_qkv_rope", "gemm_qkv_rope", "attention", "gemm_out_gate", "gemm_out_gate",
+            "ln_modulate", "gemm_mlp_up_gelu", "gemm_mlp_down_gate", "gemm_mlp_down_gate"]
+    assert got == want * 2
+    calls = bench.group_calls(got, list(range(len(got))))
+    assert [c for c, _ in calls] == ["ln_modulate", "gemm_qkv_rope", "attention", "gemm_out_gate", "ln_modulate",
+                                     "gemm_mlp_up_gelu", "gemm_mlp_down_gate"] * 2
+    assert calls[1][1] == [1, 2] and calls[6][1] == [8, 9] and calls[7][1] == [10]
+    # a 256 x 192 launch with no 256 x 256 launch of its epilogue before it starts a call of its own
+    assert bench.classify_dispatches([_row(g.format(192, 1))]) == ["gemm_mlp_up_gelu"]
+
+
 def test_traffic_lookup_rejects_stale_source(tmp_path, monkeypatch):
     rec = {"per_kernel_class": {"gemm_mlp_down_gate": {"hbm_bytes_per_launch": 123, "source_sha": "0" * 16}}}
     p = tmp_path / "t.json"
