@@ -210,7 +210,7 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_bf16_kernel(GemmPair pr, in
   int t = (blockIdx.x & 7) * per + (blockIdx.x >> 3);
   if (t >= total_tiles) return;
   int pi = t < tiles0 ? 0 : 1;
-  const GemmProblem& P = pr.p[pi];
+  const GemmProblem P = pr.p[pi];   // a copy: its fields stay in registers instead of being reloaded per use
   int tl = pi == 0 ? t : t - tiles0;
   int mt = cdiv(P.M, BM), nt = cdiv(P.N, BN);
   int tm, tn;
@@ -338,6 +338,43 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_bf16_kernel(GemmPair pr, in
     }
   };
 
+  // Epilogue inputs (bias, gate vectors, RoPE table) are requested into registers before the last
+  // k-tile, so their memory latency is covered by its MFMAs; after the loop they are written to LDS.
+  // Tiles whose inputs exceed the register budget (more than one gate row per thread or four table
+  // entries per thread) load them after the loop instead.
+  constexpr int NT = NW * 64;
+  constexpr int LDS_BYTES = 2 * (A_BYTES + W_BYTES);
+  const int rpb = (int)P.cmap.rows_per_batch;
+  const int bfirst = m0 / rpb;
+  const int nbt = (min(m0 + BM, P.M) - 1) / rpb - bfirst + 1;
+  const bool gate_lds = EPI == EPI_RESID && (size_t)(BN + nbt * BN) * 4 <= (size_t)LDS_BYTES;
+  const int rope_n = (EPI == EPI_QKV && P.rope_tab) ? P.rope_npos * (P.head_dim >> 1) : 0;
+  const bool rope_lds = rope_n > 0 && (size_t)(BN + rope_n) * 4 <= (size_t)LDS_BYTES;
+  const bool pre = (!gate_lds || nbt * BN <= NT) && (!rope_lds || rope_n <= 4 * NT);
+  // branch-free buffer loads: a lane with nothing to fetch uses an offset past num_records and reads 0
+  u16 pre_b = 0;
+  float pre_g = 0.f, pre_r[4] = {0.f, 0.f, 0.f, 0.f};
+  auto prefetch_epi = [&]() {
+    if (!pre) return;
+    const uint32_t OOB = 0x80000000u;
+    const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
+        P.bias ? (void*)P.bias : (void*)P.W, (short)0, P.bias ? P.N * 2 : 0, 0x00020000);
+    pre_b = __builtin_amdgcn_raw_buffer_load_b16(rb, tid < BN ? (uint32_t)(n0 + tid) * 2u : OOB, 0, 0);
+    if (gate_lds) {
+      const __amdgpu_buffer_rsrc_t rg = __builtin_amdgcn_make_buffer_rsrc((void*)P.gate, (short)0, 0x7fffffff, 0x00020000);
+      const int bb = tid / BN, nn = tid - bb * BN;
+      const bool ok = bb < nbt && n0 + nn < P.N;
+      pre_g = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+          rg, ok ? (uint32_t)(((int64_t)(bfirst + bb) * P.gate_bstride + n0 + nn) * 4) : OOB, 0, 0));
+    }
+    if (rope_lds) {
+      const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc((void*)P.rope_tab, (short)0, rope_n * 4, 0x00020000);
+#pragma unroll
+      for (int r = 0; r < 4; r++)
+        pre_r[r] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rr, (uint32_t)(tid + r * NT) * 4u, 0, 0));
+    }
+  };
+
   if constexpr (TRI) {
     // k-tile kt. First step: refill A stage (kt+2) % 3 with tile kt+2 (that stage last held tile
     // kt-1, whose reads ended before the previous barrier). Last step: wait for tile kt+1 (the A
@@ -393,6 +430,7 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_bf16_kernel(GemmPair pr, in
     for (int kt = 0; kt + 3 < nk; kt++) ktile3(kt, std::integral_constant<int, 0>());
     if (nk >= 3) ktile3(nk - 3, std::integral_constant<int, 1>());
     if (nk >= 2) ktile3(nk - 2, std::integral_constant<int, 2>());
+    prefetch_epi();
     ktile3(nk - 1, std::integral_constant<int, 3>());
     __builtin_amdgcn_s_setprio(0);
   } else {
@@ -403,111 +441,135 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_bf16_kernel(GemmPair pr, in
     frags(0, 0, 0);
     for (int kt = 0; kt + 2 < nk; kt++) ktile(kt, std::integral_constant<int, 0>());
     if (nk >= 2) ktile(nk - 2, std::integral_constant<int, 1>());
+    prefetch_epi();
     ktile(nk - 1, std::integral_constant<int, 2>());
   }
 
   // ---- epilogue: bias, gate vectors and the RoPE table are staged in LDS once per tile ----
-  constexpr int LDS_BYTES = 2 * (A_BYTES + W_BYTES);
-  __syncthreads();   // every wave is done with the operand tiles
-  float* s_bias = (float*)smem;                       // [BN]
-  float* s_gate = s_bias + BN;                        // [nbt][BN]
-  const int rpb = (int)P.cmap.rows_per_batch;
-  const int bfirst = m0 / rpb;
-  const int nbt = (min(m0 + BM, P.M) - 1) / rpb - bfirst + 1;
-  const bool gate_lds = EPI == EPI_RESID && (size_t)(BN + nbt * BN) * 4 <= (size_t)LDS_BYTES;
-  float* s_rope = s_bias + BN;                        // [npos][head_dim/4][2] (QKV only)
-  const int rope_n = (EPI == EPI_QKV && P.rope_tab) ? P.rope_npos * (P.head_dim >> 1) : 0;
-  const bool rope_lds = rope_n > 0 && (size_t)(BN + rope_n) * 4 <= (size_t)LDS_BYTES;
-  for (int q = tid; q < BN; q += NW * 64)
-    s_bias[q] = (P.bias && n0 + q < P.N) ? to_f32(((const u16*)P.bias)[n0 + q]) : 0.f;
-  if (gate_lds)
-    for (int q = tid; q < nbt * BN; q += NW * 64) {
-      int bb = q / BN, nn = q - bb * BN;
-      s_gate[q] = n0 + nn < P.N ? P.gate[(int64_t)(bfirst + bb) * P.gate_bstride + n0 + nn] : 0.f;
-    }
-  if (rope_lds)
-    for (int q = tid; q < rope_n; q += NW * 64) s_rope[q] = P.rope_tab[q];
-  __syncthreads();
-
   // accumulator (i, j), register r = 4 g + q (q = 0..3):
   //   MS = 32: n = 32 i + 8 g + 4 (lane / 32) + q, m = 32 j + lane % 32
   //   MS = 16: n = 16 i + 4 (lane / 16) + q,        m = 16 j + lane % 16
   constexpr int NG = NACC / 4;
   // MS = 16: the residual values of this wave's whole sub-tile (one 4-column group per block (i, j),
-  // 64 registers, free now that the fragment registers are dead) are requested at once, so their
-  // memory latency is paid once per tile instead of once per block
+  // 64 registers, free now that the fragment registers are dead) are requested at once, before the
+  // staging barriers, so their memory latency is paid once per tile and overlaps the staging
   constexpr bool XALL = EPI == EPI_RESID && MS == 16;
   uint2 xall[XALL ? TJ : 1][XALL ? TI : 1];
   if constexpr (XALL) {
+    // buffer loads, so that no load sits in a branch: a conditional load leaves the compiler unable to
+    // count the loads in flight, and it then waits for every earlier memory operation (stores
+    // included) before each use
+    const uint32_t OOB = 0x80000000u;
+    const __amdgpu_buffer_rsrc_t rc = __builtin_amdgcn_make_buffer_rsrc(P.C, (short)0, 0x7fffffff, 0x00020000);
 #pragma unroll
     for (int j = 0; j < TJ; j++) {
       const int m = m0 + wm * WTM + MS * j + frow;
-      const int64_t off = m < P.M ? row_epi(P, m).off : 0;
+      const uint32_t roff = m < P.M ? (uint32_t)(row_epi(P, m).off * 2) : OOB;
 #pragma unroll
       for (int i = 0; i < TI; i++) {
         const int n = n0 + wn * WTN + MS * i + 4 * lkc;
-        if (m < P.M && n < P.N) xall[j][i] = *(const uint2*)((const u16*)P.C + off + n);
+        const uint32_t off = (m < P.M && n < P.N) ? roff + (uint32_t)n * 2u : OOB;
+        xall[j][i] = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rc, off, 0, 0));
       }
     }
   }
+  __syncthreads();   // every wave is done with the operand tiles
+  float* s_bias = (float*)smem;                       // [BN]
+  float* s_gate = s_bias + BN;                        // [nbt][BN]
+  float* s_rope = s_bias + BN;                        // [npos][head_dim/4][2] (QKV only)
+  if (pre) {
+    if (tid < BN) s_bias[tid] = to_f32(pre_b);
+    if (gate_lds && tid < nbt * BN) s_gate[tid] = pre_g;
+    if (rope_lds) {
 #pragma unroll
-  for (int j = 0; j < TJ; j++) {
-    int m = m0 + wm * WTM + MS * j + frow;
-    if (m >= P.M) continue;
-    const RowEpi R = row_epi(P, m);
-    const int bt = m / rpb - bfirst;
-    // residual rows: prefetch the 32-column block i+1 while block i is finished
-    uint2 xr[2][4];
-    auto load_x = [&](int i, int slot) {
-#pragma unroll
-      for (int g = 0; g < NG; g++) {
-        int n = n0 + wn * WTN + MS * i + 8 * g + 4 * lkc;
-        if (EPI == EPI_RESID && n < P.N) xr[slot][g] = *(const uint2*)((const u16*)P.C + R.off + n);
+      for (int r = 0; r < 4; r++)
+        if (tid + r * NT < rope_n) s_rope[tid + r * NT] = pre_r[r];
+    }
+  } else {
+    for (int q = tid; q < BN; q += NT)
+      s_bias[q] = (P.bias && n0 + q < P.N) ? to_f32(((const u16*)P.bias)[n0 + q]) : 0.f;
+    if (gate_lds)
+      for (int q = tid; q < nbt * BN; q += NT) {
+        int bb = q / BN, nn = q - bb * BN;
+        s_gate[q] = n0 + nn < P.N ? P.gate[(int64_t)(bfirst + bb) * P.gate_bstride + n0 + nn] : 0.f;
       }
-    };
-    if (EPI == EPI_RESID && !XALL) load_x(0, 0);
+    if (rope_lds)
+      for (int q = tid; q < rope_n; q += NT) s_rope[q] = P.rope_tab[q];
+  }
+  __syncthreads();
+
+  // The store loop reads the gate vectors and the RoPE table either from LDS (STAGED) or, for tiles
+  // whose inputs did not fit the staging area, from global memory. The two are separate instances:
+  // a pointer that may point to either is a flat address, and a flat load makes the compiler wait
+  // for every store issued before it.
+  const bool rope_on = EPI == EPI_QKV && P.rope_tab != nullptr;
+  const int rope_cols = 2 * P.hidden, head_dim = P.head_dim;
+  auto store_tile = [&](auto staged_c) {
+    constexpr bool STAGED = decltype(staged_c)::value;
 #pragma unroll
-    for (int i = 0; i < TI; i++) {
-      if (EPI == EPI_RESID && !XALL && i + 1 < TI) load_x(i + 1, (i + 1) & 1);
+    for (int j = 0; j < TJ; j++) {
+      int m = m0 + wm * WTM + MS * j + frow;
+      if (m >= P.M) continue;
+      const RowEpi R = row_epi(P, m);
+      const int bt = m / rpb - bfirst;
+      // residual rows: prefetch the 32-column block i+1 while block i is finished
+      uint2 xr[2][4];
+      auto load_x = [&](int i, int slot) {
 #pragma unroll
-      for (int g = 0; g < NG; g++) {
-        int nl = wn * WTN + MS * i + 8 * g + 4 * lkc;   // column inside the tile
-        int n = n0 + nl;
-        if (n >= P.N) continue;
-        float v[4] = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
-        float4 bv = *(const float4*)(s_bias + nl);
-        v[0] += bv.x; v[1] += bv.y; v[2] += bv.z; v[3] += bv.w;
-        if (EPI == EPI_GELU) {
+        for (int g = 0; g < NG; g++) {
+          int n = n0 + wn * WTN + MS * i + 8 * g + 4 * lkc;
+          if (EPI == EPI_RESID && n < P.N) xr[slot][g] = *(const uint2*)((const u16*)P.C + R.off + n);
+        }
+      };
+      if (EPI == EPI_RESID && !XALL) load_x(0, 0);
 #pragma unroll
-          for (int q = 0; q < 4; q++) v[q] = gelu_tanh_f(v[q]);
+      for (int i = 0; i < TI; i++) {
+        if (EPI == EPI_RESID && !XALL && i + 1 < TI) load_x(i + 1, (i + 1) & 1);
+#pragma unroll
+        for (int g = 0; g < NG; g++) {
+          int nl = wn * WTN + MS * i + 8 * g + 4 * lkc;   // column inside the tile
+          int n = n0 + nl;
+          if (n >= P.N) continue;
+          float v[4] = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
+          float4 bv = *(const float4*)(s_bias + nl);
+          v[0] += bv.x; v[1] += bv.y; v[2] += bv.z; v[3] += bv.w;
+          if (EPI == EPI_GELU) {
+#pragma unroll
+            for (int q = 0; q < 4; q++) v[q] = gelu_tanh_f(v[q]);
+          }
+          if (EPI == EPI_RESID) {
+            float4 gv = STAGED ? *(const float4*)(s_gate + bt * BN + nl) : *(const float4*)(P.gate + R.gate + n);
+            uint2 u = XALL ? xall[XALL ? j : 0][XALL ? i : 0] : xr[i & 1][g];
+            v[0] = fmaf(gv.x, v[0], __uint_as_float(u.x << 16));
+            v[1] = fmaf(gv.y, v[1], __uint_as_float(u.x & 0xffff0000u));
+            v[2] = fmaf(gv.z, v[2], __uint_as_float(u.y << 16));
+            v[3] = fmaf(gv.w, v[3], __uint_as_float(u.y & 0xffff0000u));
+          }
+          if (EPI == EPI_QKV && rope_on && n < rope_cols) {
+            int dd = n & (head_dim - 1);
+            int hh = head_dim >> 1;
+            int pos = dd < hh ? R.rpos : R.cpos;
+            int pr = (dd & (hh - 1)) >> 1;
+            int ti = (pos * (head_dim >> 2) + pr) * 2;
+            float4 t = STAGED ? *(const float4*)(s_rope + ti) : *(const float4*)(P.rope_tab + ti);
+            float a0 = v[0], b0 = v[1], a1 = v[2], b1 = v[3];
+            v[0] = a0 * t.x - b0 * t.y;
+            v[1] = a0 * t.y + b0 * t.x;
+            v[2] = a1 * t.z - b1 * t.w;
+            v[3] = a1 * t.w + b1 * t.z;
+          }
+          if (OUTF32) store4<float>((float*)P.C + R.off + n, v);
+          else store4<u16>((u16*)P.C + R.off + n, v);
         }
-        if (EPI == EPI_RESID) {
-          float4 gv = gate_lds ? *(const float4*)(s_gate + bt * BN + nl)
-                               : *(const float4*)(P.gate + R.gate + n);
-          uint2 u = XALL ? xall[XALL ? j : 0][XALL ? i : 0] : xr[i & 1][g];
-          v[0] = fmaf(gv.x, v[0], __uint_as_float(u.x << 16));
-          v[1] = fmaf(gv.y, v[1], __uint_as_float(u.x & 0xffff0000u));
-          v[2] = fmaf(gv.z, v[2], __uint_as_float(u.y << 16));
-          v[3] = fmaf(gv.w, v[3], __uint_as_float(u.y & 0xffff0000u));
-        }
-        if (EPI == EPI_QKV && P.rope_tab && n < 2 * P.hidden) {
-          int dd = n & (P.head_dim - 1);
-          int hh = P.head_dim >> 1;
-          int pos = dd < hh ? R.rpos : R.cpos;
-          int pr = (dd & (hh - 1)) >> 1;
-          int ti = (pos * (P.head_dim >> 2) + pr) * 2;
-          float4 t = rope_lds ? *(const float4*)(s_rope + ti) : *(const float4*)(P.rope_tab + ti);
-          float a0 = v[0], b0 = v[1], a1 = v[2], b1 = v[3];
-          v[0] = a0 * t.x - b0 * t.y;
-          v[1] = a0 * t.y + b0 * t.x;
-          v[2] = a1 * t.z - b1 * t.w;
-          v[3] = a1 * t.w + b1 * t.z;
-        }
-        if (OUTF32) store4<float>((float*)P.C + R.off + n, v);
-        else store4<u16>((u16*)P.C + R.off + n, v);
       }
     }
-  }
+  };
+  const bool staged = (EPI != EPI_RESID || gate_lds) && (!rope_on || rope_lds);
+  // XALL: every residual load has landed before the first store. The compiler cannot order stores
+  // against loads on this counter, so inside the loop it would instead wait for earlier stores.
+  if constexpr (XALL) __builtin_amdgcn_s_waitcnt(0);
+  if (staged) store_tile(std::true_type());
+  else store_tile(std::false_type());
 #endif
 }
 
