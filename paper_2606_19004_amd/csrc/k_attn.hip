@@ -38,6 +38,26 @@ typedef __attribute__((address_space(3))) void* lds_ptr_t;
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef short i16x8 __attribute__((ext_vector_type(8)));
 
+// Combine the values of lanes l and l ^ 32 through v_permlane32_swap (a VALU exchange of the two
+// 32-lane halves) instead of an LDS permute. With both operands v, the swap's two results hold, in
+// every lane, v[l] and v[l ^ 32] (which of the two is which depends on the half), so only symmetric
+// combinations are formed from them.
+__device__ __forceinline__ void half_pair(float v, float& a, float& b) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  a = __uint_as_float(r[0]);
+  b = __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float pair_max(float v) {
+  float a, b;
+  half_pair(v, a, b);
+  return fmaxf(a, b);
+}
+__device__ __forceinline__ float pair_sum(float v) {
+  float a, b;
+  half_pair(v, a, b);
+  return a + b;
+}
+
 template <int D>
 __global__ void __launch_bounds__(256, 2) attn_fwd_bf16(AttnArgs a) {
   constexpr int QB = 128, KB = 64;
@@ -137,24 +157,25 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_bf16(AttnArgs a) {
     const char* sk = smem + buf * TILE;
     const char* sv = smem + (2 + buf) * TILE;
 
-    // S^T blocks: keys 32 kb + 8(r/4) + 4 half + r%4 of this lane's query. The K fragments of
-    // dim step s+1 are read while the MFMAs of step s run.
+    // S^T blocks: keys 32 kb + 8(r/4) + 4 half + r%4 of this lane's query. All K fragments of the
+    // tile are requested before the first score MFMA (pinned by the scheduling groups below; left to
+    // itself the compiler reused one register pair per step and waited on every read), so only the
+    // first MFMA waits for LDS.
     f32x16 st[KB / 32];
-    bf16x8 kf[2][KB / 32];
+    bf16x8 kf[NKS][KB / 32];
 #pragma unroll
-    for (int kb = 0; kb < KB / 32; kb++)
-      kf[0][kb] = *(const bf16x8*)(sk + 32 * kb * RB + krow + ((half ^ ksw) << 4));
-#pragma unroll
-    for (int s = 0; s < NKS; s++) {
-      if (s + 1 < NKS) {
-#pragma unroll
-        for (int kb = 0; kb < KB / 32; kb++)
-          kf[(s + 1) & 1][kb] = *(const bf16x8*)(sk + 32 * kb * RB + krow + (((2 * (s + 1) + half) ^ ksw) << 4));
-      }
+    for (int s = 0; s < NKS; s++)
 #pragma unroll
       for (int kb = 0; kb < KB / 32; kb++)
-        st[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s & 1][kb], qf[s], s == 0 ? zero : st[kb], 0, 0, 0);
-    }
+        kf[s][kb] = *(const bf16x8*)(sk + 32 * kb * RB + krow + (((2 * s + half) ^ ksw) << 4));
+#pragma unroll
+    for (int s = 0; s < NKS; s++)
+#pragma unroll
+      for (int kb = 0; kb < KB / 32; kb++)
+        st[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s][kb], qf[s], s == 0 ? zero : st[kb], 0, 0, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, NKS * (KB / 32), 0);   // the K fragment reads
+    __builtin_amdgcn_sched_group_barrier(0x008, NKS * (KB / 32), 0);   // then the score MFMAs
+    __builtin_amdgcn_sched_barrier(0);
     // mask keys past the end (last tile only)
     if ((kt + 1) * KB > S) {
 #pragma unroll
@@ -170,7 +191,7 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_bf16(AttnArgs a) {
     for (int kb = 0; kb < KB / 32; kb++)
 #pragma unroll
       for (int r = 0; r < 16; r++) mx = fmaxf(mx, st[kb][r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));   // the other 16 keys of each 32-key block
+    mx = pair_max(mx);   // with the other 16 keys of each 32-key block (lane ^ 32)
     const float mxs = mx * c;
     if (__ballot(mxs > m_run + TAU) != 0) {   // some row's max moved by more than TAU
       const float m_new = fmaxf(m_run, mxs);
@@ -223,7 +244,7 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_bf16(AttnArgs a) {
   }
 
   // normalise: full row sum = this lane's part + lane^32's part
-  float l_all = l_run + __shfl_xor(l_run, 32, 64);
+  float l_all = pair_sum(l_run);
   const float inv = 1.0f / l_all;
   if (qi < S) {
     u16* orow = (u16*)a.o + (int64_t)b * a.os_b + (int64_t)qi * a.os_s + (int64_t)h * a.os_h;
