@@ -482,9 +482,11 @@ size_t dit_block_workspace_bytes(const dit_block_config* cfg, int32_t batch) {
 
 namespace {
 // One block on checked arguments. mod_pre: the block's modulation computed beforehand (layout of
-// run_modulation), or null to compute it here into the workspace.
+// run_modulation), or null to compute it here into the workspace. rope_ready: the workspace already
+// holds the RoPE table (it depends only on the grid and head size, so a stack of blocks on one
+// workspace fills it once).
 dit_status block_body(const dit_block_config* c, const dit_block_weights* w, int B, const float* temb, void* x_img,
-                      void* x_txt, char* ws, const BlockWs& L, const float* mod_pre, hipStream_t s) {
+                      void* x_txt, char* ws, const BlockWs& L, const float* mod_pre, bool rope_ready, hipStream_t s) {
   dit_status st = DIT_OK;
   const int D = c->hidden, d = c->head_dim, H = c->heads;
   const int S = c->n_img + c->n_txt;
@@ -495,7 +497,8 @@ dit_status block_body(const dit_block_config* c, const dit_block_weights* w, int
   float* rope = (float*)(ws + L.rope);
 
   if (!mod_pre && (st = run_modulation(c, w, B, temb, ws, L, s))) return st;
-  if (c->rope) TIMED("small_elementwise", 0, 0, s, rope_table(rope, std::max(c->grid_h, c->grid_w), d, c->rope_theta, s));
+  if (c->rope && !rope_ready)
+    TIMED("small_elementwise", 0, 0, s, rope_table(rope, std::max(c->grid_h, c->grid_w), d, c->rope_theta, s));
   // pre-attention LN + modulate into h
   if ((st = run_ln(c, B, x_img, x_txt, mod, ws, L, 0, D, s))) return st;
   // QKV projection straight into the joint [B][S][3][H][d] buffer (+ RoPE on image q, k)
@@ -558,7 +561,8 @@ dit_status run_blocks(const dit_block_config* c, const dit_block_weights* blocks
     if (!(g0 == 0 && first_ready) && (st = run_modulation_group(c, blocks + g0, gn, B, temb, mods, inner, BL, s)))
       return st;
     for (int i = 0; i < gn; i++)
-      if ((st = block_body(c, &blocks[g0 + i], B, temb, ximg, xtxt, inner, BL, mods + i * per, s))) return st;
+      if ((st = block_body(c, &blocks[g0 + i], B, temb, ximg, xtxt, inner, BL, mods + i * per, g0 + i > 0, s)))
+        return st;
   }
   return DIT_OK;
 }
@@ -572,7 +576,7 @@ dit_status dit_block_forward(const dit_block_config* c, const dit_block_weights*
   if (st || batch == 0) return st;
   BlockWs L = block_layout(c, batch);
   if ((st = check_ws(workspace, workspace_bytes, L.total))) return st;
-  return block_body(c, w, batch, temb, x_img, x_txt, (char*)workspace, L, nullptr, hs(stream));
+  return block_body(c, w, batch, temb, x_img, x_txt, (char*)workspace, L, nullptr, false, hs(stream));
 }
 
 dit_status dit_block_mlp(const dit_block_config* c, const dit_block_weights* w, int32_t batch, const float* temb,
