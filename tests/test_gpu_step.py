@@ -29,7 +29,11 @@ def step_f64(inp, cfg):
 def run_step(d, cfg, inp):
     c = block_cfg(d, cfg)
     swd = {k: dev(v, cfg.dtype) for k, v in inp["step_weights"].items()}
-    bws = [upload_block(b, cfg.dtype) for b in inp["blocks"]]
+    up = {}   # blocks that share one weight set are uploaded once
+    for b in inp["blocks"]:
+        if id(b) not in up:
+            up[id(b)] = upload_block(b, cfg.dtype)
+    bws = [up[id(b)] for b in inp["blocks"]]
     blocks = [d.block_weights(b["img"], b["txt"]) for b in bws]
     lat = dev(inp["latent"])
     xt = dev(inp["x_txt"], cfg.dtype)
@@ -80,6 +84,35 @@ def test_step_full_shape_two_blocks_one_seed(d):
     check_step(cfg, inp, new[[3]], v[[3]], ref_new, ref_v, inp["latent"][[3]].astype(np.float64))
     # the K seeds are independent: identical inputs give identical outputs
     assert np.all(np.isfinite(new)) and np.all(np.isfinite(v))
+
+
+def test_step_nine_blocks_small(d):
+    """Nine blocks: the modulation of the first eight is computed in one batched launch (sixteen weight
+    slots) and the ninth in a group of its own, and the RoPE table is filled once for the stack;
+    compared in full against the oracle."""
+    cfg = dataclasses.replace(si.CONFIGS["small_step_bf16"], blocks=9)
+    inp = si.step_inputs(cfg)
+    new, v = run_step(d, cfg, inp)
+    ref_new, ref_v = oracle_step(cfg, inp)
+    check_step(cfg, inp, new, v, ref_new, ref_v, inp["latent"].astype(np.float64))
+
+
+def test_step_full_shape_eight_blocks_seed_permutation(d):
+    """The step in the launch configuration bench.py times (8 blocks, K=16, 1024 + 256 tokens, SDE),
+    checked through a property that holds at any size: the K seeds are processed independently, so
+    permuting the seeds of the inputs permutes the outputs, bit for bit. The 8 blocks reuse the two
+    blocks' weights of the 2-block test (the oracle check of that shape is there)."""
+    cfg = dataclasses.replace(si.CONFIGS["step_512_k16"], blocks=2)
+    inp = si.step_inputs(cfg)
+    inp["blocks"] = [inp["blocks"][i % 2] for i in range(8)]
+    cfg = dataclasses.replace(cfg, blocks=8)
+    new1, v1 = run_step(d, cfg, inp)
+    perm = np.random.default_rng(5).permutation(cfg.batch)
+    pinp = dict(inp, latent=inp["latent"][perm], eps=inp["eps"][perm], x_txt=inp["x_txt"][perm])
+    new2, v2 = run_step(d, cfg, pinp)
+    assert np.all(np.isfinite(new1)) and np.all(np.isfinite(v1))
+    np.testing.assert_array_equal(v2, v1[perm])
+    np.testing.assert_array_equal(new2, new1[perm])
 
 
 def test_step_pieces_full_shape(d):
