@@ -51,6 +51,23 @@ def test_attention_bf16_small(d, b, s, h, hd):
         assert rel_err(got[bi], ref) <= TOL_BF16
 
 
+@pytest.mark.parametrize("dtype,hd", [("bf16", 128), ("bf16", 64), ("f32", 64)])
+def test_attention_separate_tensors_head_major_output(d, dtype, hd):
+    """The general-stride boundary: q, k and v as three separate [B][S][H][d] tensors (not slices of
+    one packed buffer) and the output written head-major, [B][H][S][d], through its strides."""
+    rng = np.random.default_rng(29 + hd)
+    b, s, h = 2, 150, 3
+    qkv = [si.stored(rng.standard_normal((b, s, h, hd)).astype(np.float32), dtype) for _ in range(3)]
+    q, k, v = (dev(x, dtype) for x in qkv)
+    o = torch.full((b, h, s, hd), 7.0, dtype=q.dtype, device="cuda")
+    d.joint_attention(q, k, v, o, b, h, s, hd, (s * h * hd, h * hd, hd), (h * s * hd, hd, s * hd), dtype=dtype)
+    got = host64(o)
+    xs = [si.as_f64(x, dtype) if dtype == "bf16" else x.astype(np.float64) for x in qkv]
+    for bi in range(b):
+        ref = O.joint_attention(xs[0][bi], xs[1][bi], xs[2][bi])        # [S][H][d]
+        assert rel_err(got[bi].transpose(1, 0, 2), ref) <= (TOL_BF16 if dtype == "bf16" else TOL_F32)
+
+
 @pytest.mark.parametrize("b,s,h,hd", [(2, 80, 4, 64), (1, 45, 2, 128)])
 def test_attention_f32(d, b, s, h, hd):
     rng = np.random.default_rng(s)
