@@ -150,6 +150,50 @@ def test_block_mlp_short_k_large_tiles(d, name):
             check(cfg, g[b][rows], O.mlp_half(w64[s], m, x64), x64)
 
 
+def test_block_concurrent_host_threads_on_two_streams(d):
+    """Two host threads, each with its own stream, workspace and inputs, run block stacks at the same
+    time (different weights and seeds, one of them at the 256 x 256 tile path's size); each result
+    must equal, bit for bit, the same calls made one after the other."""
+    import threading
+    cfgs = [si.CONFIGS["small_bf16"], si.CONFIGS["mlp_short_k128"]]
+    inps = [si.block_inputs(c, seed=si.MASTER_SEED + 1 + i) for i, c in enumerate(cfgs)]
+
+    def prepare(cfg, inp):
+        c = block_cfg(d, cfg)
+        w = upload_block(inp["weights"], cfg.dtype)
+        return (c, d.block_weights(w["img"], w["txt"]), dev(inp["temb"]), dev(inp["x_img"], cfg.dtype),
+                dev(inp["x_txt"], cfg.dtype), d.workspace(d.dit_block_workspace_bytes(c, cfg.batch)), w)
+
+    def run(args, stream, reps):
+        c, bw, temb, xi, xt, ws, _ = args
+        with torch.cuda.stream(stream):
+            for _ in range(reps):
+                d.dit_block_forward(c, bw, temb, xi, xt, ws, stream=stream)
+        stream.synchronize()
+
+    reps = 3
+    seq = [prepare(c, i) for c, i in zip(cfgs, inps)]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    for a, st in zip(seq, streams):
+        run(a, st, reps)
+    par = [prepare(c, i) for c, i in zip(cfgs, inps)]
+    errs = []
+
+    def worker(a, st):
+        try:
+            run(a, st, reps)
+        except Exception as e:   # reported after the join
+            errs.append(e)
+    threads = [threading.Thread(target=worker, args=(a, st)) for a, st in zip(par, streams)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errs, errs
+    for a, b in zip(seq, par):
+        assert torch.equal(a[3], b[3]) and torch.equal(a[4], b[4])
+
+
 def test_block_errors_write_nothing(d):
     cfg = si.CONFIGS["small_bf16"]
     inp = si.block_inputs(cfg)
