@@ -618,7 +618,18 @@ static hipError_t dispatch_bf16(const GemmPair& pr, hipStream_t s) {
     big_tiles += (int64_t)cdiv(pr.p[i].M, 256) * cdiv(pr.p[i].N, 256);
   }
   if (maxn <= 64) return launch_bf16<64, 64, 2, 2, EPI, OUTF32, 32>(pr, s);
-  if (big_tiles < 512) return launch_bf16<128, 128, 2, 2, EPI, OUTF32, 32>(pr, s);
+  // 128 x 128 tiles (4 waves, two workgroups per CU) or 256 x 256 tiles (8 waves, one per CU): the
+  // one with fewer estimated rounds, a round of 2 x CUs small tiles costing C128 of a large round
+  // (a quarter of the flops per tile, at lower MFMA efficiency)
+  {
+    constexpr double C128 = 0.71;
+    const int64_t cus = cu_count();
+    int64_t small_tiles = 0;
+    for (int i = 0; i < pr.nprob; i++) small_tiles += (int64_t)cdiv(pr.p[i].M, 128) * cdiv(pr.p[i].N, 128);
+    const double big = (double)((big_tiles + cus - 1) / cus);
+    const double small = C128 * (double)((small_tiles + 2 * cus - 1) / (2 * cus));
+    if (small < big) return launch_bf16<128, 128, 2, 2, EPI, OUTF32, 32>(pr, s);
+  }
   // large problems: 8 waves of 64x128 on 16x16x32 MFMAs (measured 3-7% faster than 32x32x16 here),
   // with three A stages, so the activation rows are requested two k-tiles ahead (in the denoise step
   // every block's weights and most activation panels arrive cold from HBM).
