@@ -27,7 +27,9 @@
  *     fp32 epilogue math; DIT_F32 = fp32 throughout. temb, the latent, the
  *     velocity, noise and rewards are always fp32.
  *   - Thread safety: no mutable global state besides the per-thread error
- *     text; calls on different streams with disjoint buffers may overlap.
+ *     text and per-device caches filled once (atomics: the device's compute
+ *     unit count and the kernels' LDS limits); calls on different streams
+ *     with disjoint buffers may overlap, also on their first call.
  */
 #ifndef DITSTEP_H
 #define DITSTEP_H
@@ -128,6 +130,12 @@ const char* dit_last_error_message(void);
 size_t dit_block_workspace_bytes(const dit_block_config* cfg, int32_t batch);
 
 /* One dual-stream MMDiT block, in place on both residual streams.
+ * Source: every denoising step of the rollout is one full forward pass of the DiT
+ * backbone, run for the K seeds of a prompt group (section 2.1, "Diffusion Models and
+ * DiT RL Post-Training"); the backbone is Qwen-Image, a 20B MMDiT (section 6.1, "Model
+ * Setup"). The paper does not restate the block, so its internals below (adaLN
+ * modulation, joint attention, GELU-tanh MLP) are the dual-stream MMDiT reading, and
+ * the sizes are those of the workloads the paper runs (512x512 and 1280x1280 images).
  *   temb  [B][D] fp32        per-sample conditioning vector
  *   x_img [B][N_i][D]        image residual stream (in/out), config dtype
  *   x_txt [B][N_t][D]        text residual stream (in/out), config dtype
@@ -150,6 +158,11 @@ dit_status dit_block_mlp(const dit_block_config* cfg, const dit_block_weights* w
 
 /* Joint non-causal multi-head attention, o = softmax(q k^T * scale) v per
  * (sample, head), every query attending to all `seq` keys.
+ * Source: the attention inside each block of the DiT forward pass (section 2.1); at
+ * 1280x1280 the paper splits it over a sequence-parallel group (sections 2.1 and 4.4,
+ * SP=2 in section 6.1), and one rank's share is a subset of the heads over the whole
+ * sequence, which is what the head stride here addresses. Text and image tokens form one
+ * sequence with no mask (the joint attention of an MMDiT; the paper does not restate it).
  * q, k, v: element (b, s, h, e) at base + b*qkv_stride_b + s*qkv_stride_s +
  *   h*qkv_stride_h + e (strides in ELEMENTS, e contiguous), so q/k/v may be
  *   slices of one packed [B][S][3][H][d] buffer.

@@ -3,6 +3,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <atomic>
 #include <cstring>
 #include <limits>
 #include <map>
@@ -12,42 +13,17 @@
 
 #include "../../include/ditstep.h"
 #include "internal.h"
-#include "status.h"
+#include "host_checks.h"
 
 using namespace dit;
-
-namespace {
-
-thread_local std::string g_err;
-
-dit_status fail(dit_status s, const char* fmt, ...) {
-  char buf[512];
-  va_list ap;
-  va_start(ap, fmt);
-  vsnprintf(buf, sizeof buf, fmt, ap);
-  va_end(ap);
-  g_err = buf;
-  return s;
-}
-
-}  // namespace
-
-dit_status dit::set_error(dit_status s, const char* fmt, ...) {
-  char buf[512];
-  va_list ap;
-  va_start(ap, fmt);
-  vsnprintf(buf, sizeof buf, fmt, ap);
-  va_end(ap);
-  g_err = buf;
-  return s;
-}
+using dit::set_error;
 
 namespace {
 
 #define HIP_TRY(expr)                                                                         \
   do {                                                                                        \
     hipError_t e_ = (expr);                                                                   \
-    if (e_ != hipSuccess) return fail(DIT_ERR_HIP, "%s failed: %s", #expr, hipGetErrorString(e_)); \
+    if (e_ != hipSuccess) return set_error(DIT_ERR_HIP, "%s failed: %s", #expr, hipGetErrorString(e_)); \
   } while (0)
 
 // ---- opt-in kernel timing (dit_profile_begin / dit_profile_end) ----
@@ -58,14 +34,14 @@ struct ProfRec {
 };
 struct Prof {
   std::mutex mu;
-  bool on = false;
+  std::atomic<bool> on{false};   // read without the lock on every launch
   std::vector<ProfRec> recs;
 };
 Prof g_prof;
 
 template <class F>
 hipError_t timed(const char* name, double flops, double bytes, hipStream_t s, F&& launch) {
-  if (!g_prof.on) return launch();
+  if (!g_prof.on.load(std::memory_order_acquire)) return launch();
   hipEvent_t a, b;
   hipError_t e = hipEventCreate(&a);
   if (e != hipSuccess) return e;
@@ -90,30 +66,11 @@ inline bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 inline size_t esize(int32_t dtype) { return dtype == DIT_BF16 ? 2 : 4; }
 inline hipStream_t hs(dit_stream s) { return (hipStream_t)s; }
 
-dit_status check_config(const dit_block_config* c) {
-  if (!c) return fail(DIT_ERR_INVALID_ARG, "config is NULL");
-  if (c->dtype != DIT_F32 && c->dtype != DIT_BF16) return fail(DIT_ERR_INVALID_ARG, "dtype %d invalid", c->dtype);
-  if (c->hidden <= 0 || c->heads <= 0 || c->head_dim <= 0 || c->mlp_hidden <= 0)
-    return fail(DIT_ERR_SHAPE, "hidden/heads/head_dim/mlp_hidden must be positive");
-  if (c->hidden != c->heads * c->head_dim)
-    return fail(DIT_ERR_SHAPE, "hidden %d != heads %d * head_dim %d", c->hidden, c->heads, c->head_dim);
-  if (c->head_dim != 64 && c->head_dim != 128) return fail(DIT_ERR_UNSUPPORTED, "head_dim %d (64 or 128)", c->head_dim);
-  if (c->hidden % 64 || c->mlp_hidden % 64) return fail(DIT_ERR_UNSUPPORTED, "hidden and mlp_hidden must be multiples of 64");
-  if (c->hidden > 4096) return fail(DIT_ERR_UNSUPPORTED, "hidden %d > 4096", c->hidden);
-  if (c->grid_h <= 0 || c->grid_w <= 0 || c->n_img != c->grid_h * c->grid_w)
-    return fail(DIT_ERR_SHAPE, "n_img %d != grid_h %d * grid_w %d", c->n_img, c->grid_h, c->grid_w);
-  if (c->n_txt < 0) return fail(DIT_ERR_SHAPE, "n_txt %d < 0", c->n_txt);
-  if (!(c->ln_eps > 0.f) || !std::isfinite(c->ln_eps)) return fail(DIT_ERR_INVALID_ARG, "ln_eps must be positive");
-  if (c->rope && (!(c->rope_theta > 0.f) || !std::isfinite(c->rope_theta)))
-    return fail(DIT_ERR_INVALID_ARG, "rope_theta must be positive");
-  return DIT_OK;
-}
-
 dit_status check_ws(void* ws, size_t have, size_t need) {
   if (need == 0) return DIT_OK;
-  if (!ws) return fail(DIT_ERR_WORKSPACE, "workspace is NULL (%zu bytes needed)", need);
-  if ((uintptr_t)ws & 255) return fail(DIT_ERR_WORKSPACE, "workspace not 256-byte aligned");
-  if (have < need) return fail(DIT_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", have, need);
+  if (!ws) return set_error(DIT_ERR_WORKSPACE, "workspace is NULL (%zu bytes needed)", need);
+  if ((uintptr_t)ws & 255) return set_error(DIT_ERR_WORKSPACE, "workspace not 256-byte aligned");
+  if (have < need) return set_error(DIT_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", have, need);
   return DIT_OK;
 }
 
@@ -144,25 +101,26 @@ dit_status check_block_args(const dit_block_config* c, const dit_block_weights* 
                             const float* temb, void* x_img, void* x_txt) {
   dit_status st = check_config(c);
   if (st) return st;
-  if (!w) return fail(DIT_ERR_INVALID_ARG, "weights is NULL");
-  if (batch < 0) return fail(DIT_ERR_INVALID_ARG, "batch %d < 0", batch);
+  if (!w) return set_error(DIT_ERR_INVALID_ARG, "weights is NULL");
+  if (batch < 0) return set_error(DIT_ERR_INVALID_ARG, "batch %d < 0", batch);
   if (batch == 0) return DIT_OK;
-  if (!temb || !x_img || (c->n_txt > 0 && !x_txt)) return fail(DIT_ERR_INVALID_ARG, "temb/x_img/x_txt NULL");
+  if (!temb || !x_img || (c->n_txt > 0 && !x_txt)) return set_error(DIT_ERR_INVALID_ARG, "temb/x_img/x_txt NULL");
   if (!aligned16(temb) || !aligned16(x_img) || (x_txt && !aligned16(x_txt)))
-    return fail(DIT_ERR_INVALID_ARG, "temb/x_img/x_txt must be 16-byte aligned");
+    return set_error(DIT_ERR_INVALID_ARG, "temb/x_img/x_txt must be 16-byte aligned");
   for (int s = 0; s < 2; s++) {
     if (!w->mod_w[s] || !w->qkv_w[s] || !w->out_w[s] || !w->mlp1_w[s] || !w->mlp2_w[s])
-      return fail(DIT_ERR_INVALID_ARG, "a weight matrix of stream %d is NULL", s);
+      return set_error(DIT_ERR_INVALID_ARG, "a weight matrix of stream %d is NULL", s);
     const void* all[10] = {w->mod_w[s], w->mod_b[s], w->qkv_w[s], w->qkv_b[s], w->out_w[s],
                            w->out_b[s], w->mlp1_w[s], w->mlp1_b[s], w->mlp2_w[s], w->mlp2_b[s]};
     for (const void* p : all)
-      if (p && ((uintptr_t)p & 7)) return fail(DIT_ERR_INVALID_ARG, "weights must be 8-byte aligned");
+      if (p && ((uintptr_t)p & 7)) return set_error(DIT_ERR_INVALID_ARG, "weights must be 8-byte aligned");
   }
-  // the MFMA GEMM addresses its A operand with 31-bit byte offsets
-  if (c->dtype == DIT_BF16) {
+  // the MFMA GEMM addresses its A operand with 31-bit byte offsets, and row counts (B x S) are 32-bit
+  // in both paths: the largest activation buffer stays below 2 GiB
+  {
     double S = (double)c->n_img + c->n_txt;
-    double big = (double)batch * S * std::max(3 * c->hidden, c->mlp_hidden) * 2.0;
-    if (big >= 2147483648.0) return fail(DIT_ERR_UNSUPPORTED, "activation buffer of %.0f bytes exceeds 2 GiB", big);
+    double big = (double)batch * S * std::max(3 * c->hidden, c->mlp_hidden) * (double)esize(c->dtype);
+    if (big >= 2147483648.0) return set_error(DIT_ERR_UNSUPPORTED, "activation buffer of %.0f bytes exceeds 2 GiB", big);
   }
   return DIT_OK;
 }
@@ -332,9 +290,9 @@ StepWs step_layout(const dit_block_config* c, int64_t B, int C) {
 }
 
 dit_status check_step_weights(const dit_step_weights* w) {
-  if (!w) return fail(DIT_ERR_INVALID_ARG, "step weights NULL");
+  if (!w) return set_error(DIT_ERR_INVALID_ARG, "step weights NULL");
   if (!w->t1_w || !w->t2_w || !w->in_w || !w->fmod_w || !w->fout_w)
-    return fail(DIT_ERR_INVALID_ARG, "a step weight matrix is NULL");
+    return set_error(DIT_ERR_INVALID_ARG, "a step weight matrix is NULL");
   return DIT_OK;
 }
 
@@ -425,53 +383,12 @@ dit_status run_final(const dit_block_config* c, const dit_step_weights* w, int B
   return DIT_OK;
 }
 
-dit_status flow_coefficients(float t, float t_next, float a, bool has_noise, float* cx, float* cv, float* ce) {
-  if (!std::isfinite(t) || !std::isfinite(t_next) || !std::isfinite(a) || a < 0.f)
-    return fail(DIT_ERR_DOMAIN, "t, t_next and noise_level must be finite, noise_level >= 0");
-  if (t_next > t) return fail(DIT_ERR_DOMAIN, "t_next %g > t %g (the sampler runs from noise t=1 to data t=0)", t_next, t);
-  double h = (double)t_next - (double)t;
-  if (a == 0.f) {
-    *cx = 1.f;
-    *cv = (float)h;
-    *ce = 0.f;
-    return DIT_OK;
-  }
-  if (!(t > 0.f && t < 1.f)) return fail(DIT_ERR_DOMAIN, "SDE step needs 0 < t < 1 (t = %g)", t);
-  if (t_next < 0.f) return fail(DIT_ERR_DOMAIN, "t_next %g < 0", t_next);
-  if (!has_noise) return fail(DIT_ERR_INVALID_ARG, "noise is NULL with noise_level > 0");
-  double td = t, sigma = (double)a * std::sqrt(td / (1.0 - td));
-  double k = sigma * sigma / (2.0 * td);
-  // x + h (v + k (x + (1-t) v)) + sigma sqrt(-h) eps  =  (1 + h k) x + h (1 + k (1-t)) v + sigma sqrt(-h) eps
-  *cx = (float)(1.0 + h * k);
-  *cv = (float)(h * (1.0 + k * (1.0 - td)));
-  *ce = (float)(sigma * std::sqrt(-h));
-  return DIT_OK;
-}
-
 }  // namespace
 
 // ===========================================================================
 // exported entry points
 // ===========================================================================
 extern "C" {
-
-int32_t dit_abi_version(void) { return DIT_ABI_VERSION; }
-
-const char* dit_status_string(dit_status s) {
-  switch (s) {
-    case DIT_OK: return "ok";
-    case DIT_ERR_INVALID_ARG: return "invalid argument";
-    case DIT_ERR_SHAPE: return "inconsistent shape";
-    case DIT_ERR_DOMAIN: return "argument outside the domain";
-    case DIT_ERR_NAN: return "NaN or infinite input";
-    case DIT_ERR_UNSUPPORTED: return "unsupported configuration";
-    case DIT_ERR_HIP: return "HIP runtime error";
-    case DIT_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
-  }
-  return "unknown status";
-}
-
-const char* dit_last_error_message(void) { return g_err.c_str(); }
 
 size_t dit_block_workspace_bytes(const dit_block_config* cfg, int32_t batch) {
   if (check_config(cfg) != DIT_OK || batch < 0) return 0;
@@ -594,21 +511,21 @@ dit_status joint_attention(const void* q, const void* k, const void* v, void* o,
                            int32_t seq, int32_t head_dim, int64_t qkv_stride_b, int64_t qkv_stride_s,
                            int64_t qkv_stride_h, int64_t o_stride_b, int64_t o_stride_s, int64_t o_stride_h,
                            float scale, int32_t dtype, dit_stream stream) {
-  if (dtype != DIT_F32 && dtype != DIT_BF16) return fail(DIT_ERR_INVALID_ARG, "dtype %d invalid", dtype);
-  if (batch < 0 || heads < 0 || seq < 0) return fail(DIT_ERR_INVALID_ARG, "negative size");
-  if (head_dim != 64 && head_dim != 128) return fail(DIT_ERR_UNSUPPORTED, "head_dim %d (64 or 128)", head_dim);
+  if (dtype != DIT_F32 && dtype != DIT_BF16) return set_error(DIT_ERR_INVALID_ARG, "dtype %d invalid", dtype);
+  if (batch < 0 || heads < 0 || seq < 0) return set_error(DIT_ERR_INVALID_ARG, "negative size");
+  if (head_dim != 64 && head_dim != 128) return set_error(DIT_ERR_UNSUPPORTED, "head_dim %d (64 or 128)", head_dim);
   if ((int64_t)batch * heads * seq == 0) return DIT_OK;
-  if (!q || !k || !v || !o) return fail(DIT_ERR_INVALID_ARG, "q/k/v/o NULL");
-  if (!std::isfinite(scale)) return fail(DIT_ERR_INVALID_ARG, "scale not finite");
+  if (!q || !k || !v || !o) return set_error(DIT_ERR_INVALID_ARG, "q/k/v/o NULL");
+  if (!std::isfinite(scale)) return set_error(DIT_ERR_INVALID_ARG, "scale not finite");
   size_t es = esize(dtype);
   const int64_t strides[6] = {qkv_stride_b, qkv_stride_s, qkv_stride_h, o_stride_b, o_stride_s, o_stride_h};
   for (int64_t st : strides)
-    if (st < 0 || (st * (int64_t)es) % 16) return fail(DIT_ERR_INVALID_ARG, "strides must be >= 0 and keep 16-byte rows");
+    if (st < 0 || (st * (int64_t)es) % 16) return set_error(DIT_ERR_INVALID_ARG, "strides must be >= 0 and keep 16-byte rows");
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o))
-    return fail(DIT_ERR_INVALID_ARG, "q/k/v/o must be 16-byte aligned");
+    return set_error(DIT_ERR_INVALID_ARG, "q/k/v/o must be 16-byte aligned");
   // the bf16 kernel addresses the keys of one (sample, head) with 31-bit byte offsets
   if (dtype == DIT_BF16 && (double)seq * qkv_stride_s * 2.0 >= 2147483648.0)
-    return fail(DIT_ERR_UNSUPPORTED, "seq * qkv_stride_s spans more than 2 GiB");
+    return set_error(DIT_ERR_UNSUPPORTED, "seq * qkv_stride_s spans more than 2 GiB");
   AttnArgs a{};
   a.q = q;
   a.k = k;
@@ -631,12 +548,12 @@ dit_status joint_attention(const void* q, const void* k, const void* v, void* o,
 
 dit_status flow_step(float* x, const float* v, const float* noise, int64_t n, float t, float t_next,
                      float noise_level, dit_stream stream) {
-  if (n < 0) return fail(DIT_ERR_INVALID_ARG, "n %lld < 0", (long long)n);
+  if (n < 0) return set_error(DIT_ERR_INVALID_ARG, "n %lld < 0", (long long)n);
   float cx, cv, ce;
   dit_status st = flow_coefficients(t, t_next, noise_level, noise != nullptr, &cx, &cv, &ce);
   if (st) return st;
   if (n == 0) return DIT_OK;
-  if (!x || !v) return fail(DIT_ERR_INVALID_ARG, "x/v NULL");
+  if (!x || !v) return set_error(DIT_ERR_INVALID_ARG, "x/v NULL");
   TIMED("flow_step", 0, (noise_level > 0.f ? 16.0 : 12.0) * n, hs(stream), flow_update(x, v, noise_level > 0.f ? noise : nullptr, n, cx, cv, ce, hs(stream)));
   return DIT_OK;
 }
@@ -644,14 +561,14 @@ dit_status flow_step(float* x, const float* v, const float* noise, int64_t n, fl
 dit_status flow_logprob(const float* x, const float* v, const float* x_next, int32_t batch, int64_t n_per_sample,
                         float t, float t_next, float noise_level, double* logp, dit_stream stream) {
   if (batch < 0 || n_per_sample < 0)
-    return fail(DIT_ERR_INVALID_ARG, "batch %d / n_per_sample %lld < 0", batch, (long long)n_per_sample);
+    return set_error(DIT_ERR_INVALID_ARG, "batch %d / n_per_sample %lld < 0", batch, (long long)n_per_sample);
   if (!(noise_level > 0.f) || !std::isfinite(noise_level))
-    return fail(DIT_ERR_DOMAIN, "flow_logprob needs a finite noise_level > 0 (the ODE step has no density)");
+    return set_error(DIT_ERR_DOMAIN, "flow_logprob needs a finite noise_level > 0 (the ODE step has no density)");
   if (!(t > 0.f && t < 1.f) || !std::isfinite(t_next) || !(t_next < t))
-    return fail(DIT_ERR_DOMAIN, "flow_logprob needs 0 < t < 1 and t_next < t (t=%g, t_next=%g)", t, t_next);
+    return set_error(DIT_ERR_DOMAIN, "flow_logprob needs 0 < t < 1 and t_next < t (t=%g, t_next=%g)", t, t_next);
   if (batch == 0) return DIT_OK;
-  if (!logp) return fail(DIT_ERR_INVALID_ARG, "logp NULL");
-  if (n_per_sample > 0 && (!x || !v || !x_next)) return fail(DIT_ERR_INVALID_ARG, "x/v/x_next NULL");
+  if (!logp) return set_error(DIT_ERR_INVALID_ARG, "logp NULL");
+  if (n_per_sample > 0 && (!x || !v || !x_next)) return set_error(DIT_ERR_INVALID_ARG, "x/v/x_next NULL");
   const double td = t, h = (double)t_next - td, a = noise_level;
   const double var = a * a * td / (1.0 - td) * (-h);
   const double k1 = 0.5 * a * a / (1.0 - td);           // sigma^2 / (2t)
@@ -664,19 +581,19 @@ dit_status flow_logprob(const float* x, const float* v, const float* x_next, int
 dit_status group_reward_stats(const float* rewards, int32_t groups, int32_t n, float adv_eps, int32_t k_select,
                               float* mean, float* stdv, float* adv, int32_t* order, int32_t* selected,
                               dit_stream stream) {
-  if (groups < 0) return fail(DIT_ERR_INVALID_ARG, "groups %d < 0", groups);
-  if (n < 1 || n > 4096) return fail(DIT_ERR_INVALID_ARG, "n %d outside [1, 4096]", n);
-  if (k_select < 0 || k_select > n) return fail(DIT_ERR_INVALID_ARG, "k_select %d outside [0, n=%d]", k_select, n);
-  if (!(adv_eps >= 0.f) || !std::isfinite(adv_eps)) return fail(DIT_ERR_INVALID_ARG, "adv_eps must be >= 0");
+  if (groups < 0) return set_error(DIT_ERR_INVALID_ARG, "groups %d < 0", groups);
+  if (n < 1 || n > 4096) return set_error(DIT_ERR_INVALID_ARG, "n %d outside [1, 4096]", n);
+  if (k_select < 0 || k_select > n) return set_error(DIT_ERR_INVALID_ARG, "k_select %d outside [0, n=%d]", k_select, n);
+  if (!(adv_eps >= 0.f) || !std::isfinite(adv_eps)) return set_error(DIT_ERR_INVALID_ARG, "adv_eps must be >= 0");
   if (groups == 0) return DIT_OK;
-  if (!rewards) return fail(DIT_ERR_INVALID_ARG, "rewards NULL");
+  if (!rewards) return set_error(DIT_ERR_INVALID_ARG, "rewards NULL");
   hipStream_t s = hs(stream);
   // NaN / Inf check on a host copy of the (small) input, before anything is written
   std::vector<float> host((size_t)groups * n);
   HIP_TRY(hipMemcpyAsync(host.data(), rewards, host.size() * 4, hipMemcpyDeviceToHost, s));
   HIP_TRY(hipStreamSynchronize(s));
   for (size_t i = 0; i < host.size(); i++)
-    if (!std::isfinite(host[i])) return fail(DIT_ERR_NAN, "reward %zu (group %zu) is not finite", i % n, i / n);
+    if (!std::isfinite(host[i])) return set_error(DIT_ERR_NAN, "reward %zu (group %zu) is not finite", i % n, i / n);
   TIMED("reward_stats", 0, 4.0 * groups * n, s, reward_stats(rewards, groups, n, adv_eps, k_select, mean, stdv, adv, order, selected, s));
   return DIT_OK;
 }
@@ -685,9 +602,9 @@ dit_status dit_timestep_embed(const dit_block_config* c, const dit_step_weights*
                               float* temb, void* workspace, size_t workspace_bytes, dit_stream stream) {
   dit_status st = check_config(c);
   if (st || (st = check_step_weights(w))) return st;
-  if (batch < 0) return fail(DIT_ERR_INVALID_ARG, "batch < 0");
+  if (batch < 0) return set_error(DIT_ERR_INVALID_ARG, "batch < 0");
   if (batch == 0) return DIT_OK;
-  if (!t || !temb) return fail(DIT_ERR_INVALID_ARG, "t/temb NULL");
+  if (!t || !temb) return set_error(DIT_ERR_INVALID_ARG, "t/temb NULL");
   if ((st = check_ws(workspace, workspace_bytes, timestep_ws(c, batch)))) return st;
   return run_timestep(c, w, batch, t, 0.f, temb, (char*)workspace, hs(stream));
 }
@@ -697,11 +614,11 @@ dit_status dit_patch_embed(const dit_block_config* c, const dit_step_weights* w,
                            dit_stream stream) {
   dit_status st = check_config(c);
   if (st || (st = check_step_weights(w))) return st;
-  if (batch < 0) return fail(DIT_ERR_INVALID_ARG, "batch < 0");
-  if (latent_dim <= 0 || latent_dim % 64) return fail(DIT_ERR_UNSUPPORTED, "latent_dim %d (multiple of 64)", latent_dim);
+  if (batch < 0) return set_error(DIT_ERR_INVALID_ARG, "batch < 0");
+  if (latent_dim <= 0 || latent_dim % 64) return set_error(DIT_ERR_UNSUPPORTED, "latent_dim %d (multiple of 64)", latent_dim);
   if (batch == 0) return DIT_OK;
   if (!latent || !x_img || !aligned16(latent) || !aligned16(x_img))
-    return fail(DIT_ERR_INVALID_ARG, "latent/x_img NULL or not 16-byte aligned");
+    return set_error(DIT_ERR_INVALID_ARG, "latent/x_img NULL or not 16-byte aligned");
   if ((st = check_ws(workspace, workspace_bytes, patch_ws(c, batch, latent_dim)))) return st;
   return run_patch(c, w, batch, latent_dim, latent, x_img, (char*)workspace, hs(stream));
 }
@@ -711,11 +628,11 @@ dit_status dit_final_layer(const dit_block_config* c, const dit_step_weights* w,
                            dit_stream stream) {
   dit_status st = check_config(c);
   if (st || (st = check_step_weights(w))) return st;
-  if (batch < 0) return fail(DIT_ERR_INVALID_ARG, "batch < 0");
-  if (latent_dim <= 0 || latent_dim % 64) return fail(DIT_ERR_UNSUPPORTED, "latent_dim %d (multiple of 64)", latent_dim);
+  if (batch < 0) return set_error(DIT_ERR_INVALID_ARG, "batch < 0");
+  if (latent_dim <= 0 || latent_dim % 64) return set_error(DIT_ERR_UNSUPPORTED, "latent_dim %d (multiple of 64)", latent_dim);
   if (batch == 0) return DIT_OK;
   if (!temb || !x_img || !v || !aligned16(temb) || !aligned16(x_img) || !aligned16(v))
-    return fail(DIT_ERR_INVALID_ARG, "temb/x_img/v NULL or not 16-byte aligned");
+    return set_error(DIT_ERR_INVALID_ARG, "temb/x_img/v NULL or not 16-byte aligned");
   if ((st = check_ws(workspace, workspace_bytes, final_ws(c, batch)))) return st;
   return run_final(c, w, batch, latent_dim, temb, x_img, v, (char*)workspace, hs(stream));
 }
@@ -731,15 +648,15 @@ dit_status dit_denoise_step(const dit_block_config* c, const dit_step_weights* s
                             void* workspace, size_t workspace_bytes, dit_stream stream) {
   dit_status st = check_config(c);
   if (st || (st = check_step_weights(sw))) return st;
-  if (n_blocks < 0 || (n_blocks > 0 && !blocks)) return fail(DIT_ERR_INVALID_ARG, "blocks NULL or n_blocks < 0");
-  if (batch < 0) return fail(DIT_ERR_INVALID_ARG, "batch < 0");
-  if (latent_dim <= 0 || latent_dim % 64) return fail(DIT_ERR_UNSUPPORTED, "latent_dim %d (multiple of 64)", latent_dim);
+  if (n_blocks < 0 || (n_blocks > 0 && !blocks)) return set_error(DIT_ERR_INVALID_ARG, "blocks NULL or n_blocks < 0");
+  if (batch < 0) return set_error(DIT_ERR_INVALID_ARG, "batch < 0");
+  if (latent_dim <= 0 || latent_dim % 64) return set_error(DIT_ERR_UNSUPPORTED, "latent_dim %d (multiple of 64)", latent_dim);
   float cx, cv, ce;
   if ((st = flow_coefficients(t, t_next, noise_level, noise != nullptr, &cx, &cv, &ce))) return st;
   if (batch == 0) return DIT_OK;
   if (!latent || !aligned16(latent) || (c->n_txt > 0 && (!x_txt || !aligned16(x_txt))) ||
       (v_out && !aligned16(v_out)))
-    return fail(DIT_ERR_INVALID_ARG, "latent/x_txt/v_out NULL or not 16-byte aligned");
+    return set_error(DIT_ERR_INVALID_ARG, "latent/x_txt/v_out NULL or not 16-byte aligned");
   StepWs L = step_layout(c, batch, latent_dim);
   if ((st = check_ws(workspace, workspace_bytes, L.total))) return st;
   char* ws = (char*)workspace;
@@ -784,44 +701,6 @@ TeaCacheLayout teacache_layout(const dit_block_config* c, int64_t B) {
 }
 }  // namespace
 
-dit_status dit_teacache_init(dit_teacache_state* st, double threshold, const double* coef, int32_t n_coef) {
-  if (!st) return fail(DIT_ERR_INVALID_ARG, "state is NULL");
-  if (!(threshold >= 0.0) || !std::isfinite(threshold)) return fail(DIT_ERR_INVALID_ARG, "threshold %g < 0", threshold);
-  if (n_coef < 0 || n_coef > 8 || (n_coef > 0 && !coef)) return fail(DIT_ERR_INVALID_ARG, "n_coef %d (0..8)", n_coef);
-  std::memset(st, 0, sizeof *st);
-  st->threshold = threshold;
-  st->n_coef = n_coef;
-  for (int i = 0; i < n_coef; i++) {
-    if (!std::isfinite(coef[i])) return fail(DIT_ERR_INVALID_ARG, "coef[%d] not finite", i);
-    st->coef[i] = coef[i];
-  }
-  return DIT_OK;
-}
-
-dit_status dit_teacache_gate(dit_teacache_state* st, double rel, int32_t force, int32_t* run_blocks) {
-  if (!st || !run_blocks) return fail(DIT_ERR_INVALID_ARG, "state / run_blocks is NULL");
-  if (st->n_coef < 0 || st->n_coef > 8) return fail(DIT_ERR_INVALID_ARG, "state n_coef %d (0..8)", st->n_coef);
-  if (force || !st->has_prev || !st->has_residual) {
-    st->accumulated = 0.0;
-    *run_blocks = 1;
-    return DIT_OK;
-  }
-  if (!std::isfinite(rel)) return fail(DIT_ERR_NAN, "distance %g is not finite", rel);
-  double v = rel;
-  if (st->n_coef > 0) {   // Horner, highest power first
-    v = 0.0;
-    for (int i = 0; i < st->n_coef; i++) v = v * rel + st->coef[i];
-  }
-  st->accumulated += v;
-  if (st->accumulated < st->threshold) {
-    *run_blocks = 0;
-  } else {
-    st->accumulated = 0.0;
-    *run_blocks = 1;
-  }
-  return DIT_OK;
-}
-
 size_t dit_teacache_cache_bytes(const dit_block_config* c, int32_t batch) {
   if (check_config(c) != DIT_OK || batch < 0) return 0;
   return teacache_layout(c, batch).total;
@@ -835,19 +714,19 @@ dit_status dit_denoise_step_teacache(const dit_block_config* c, const dit_step_w
                                      void* workspace, size_t workspace_bytes, dit_stream stream) {
   dit_status st = check_config(c);
   if (st || (st = check_step_weights(sw))) return st;
-  if (n_blocks < 1 || !blocks) return fail(DIT_ERR_INVALID_ARG, "the gated step needs n_blocks >= 1");
-  if (!state) return fail(DIT_ERR_INVALID_ARG, "state is NULL");
-  if (batch < 0) return fail(DIT_ERR_INVALID_ARG, "batch < 0");
-  if (latent_dim <= 0 || latent_dim % 64) return fail(DIT_ERR_UNSUPPORTED, "latent_dim %d (multiple of 64)", latent_dim);
+  if (n_blocks < 1 || !blocks) return set_error(DIT_ERR_INVALID_ARG, "the gated step needs n_blocks >= 1");
+  if (!state) return set_error(DIT_ERR_INVALID_ARG, "state is NULL");
+  if (batch < 0) return set_error(DIT_ERR_INVALID_ARG, "batch < 0");
+  if (latent_dim <= 0 || latent_dim % 64) return set_error(DIT_ERR_UNSUPPORTED, "latent_dim %d (multiple of 64)", latent_dim);
   float cx, cv, ce;
   if ((st = flow_coefficients(t, t_next, noise_level, noise != nullptr, &cx, &cv, &ce))) return st;
   if (batch == 0) return DIT_OK;
   if (!latent || !aligned16(latent) || (c->n_txt > 0 && (!x_txt || !aligned16(x_txt))) ||
       (v_out && !aligned16(v_out)))
-    return fail(DIT_ERR_INVALID_ARG, "latent/x_txt/v_out NULL or not 16-byte aligned");
+    return set_error(DIT_ERR_INVALID_ARG, "latent/x_txt/v_out NULL or not 16-byte aligned");
   const TeaCacheLayout TL = teacache_layout(c, batch);
   if (!cache || !aligned16(cache) || cache_bytes < TL.total)
-    return fail(DIT_ERR_WORKSPACE, "cache %zu bytes < %zu or not aligned", cache_bytes, TL.total);
+    return set_error(DIT_ERR_WORKSPACE, "cache %zu bytes < %zu or not aligned", cache_bytes, TL.total);
   StepWs L = step_layout(c, batch, latent_dim);
   if ((st = check_ws(workspace, workspace_bytes, L.total))) return st;
   char* ws = (char*)workspace;
@@ -917,13 +796,13 @@ dit_status dit_profile_begin(void) {
     (void)hipEventDestroy(r.b);
   }
   g_prof.recs.clear();
-  g_prof.on = true;
+  g_prof.on.store(true, std::memory_order_release);
   return DIT_OK;
 }
 
 dit_status dit_profile_end(dit_kernel_stat* stats, int32_t capacity, int32_t* count) {
   std::lock_guard<std::mutex> g(g_prof.mu);
-  g_prof.on = false;
+  g_prof.on.store(false, std::memory_order_release);
   std::map<std::string, dit_kernel_stat> agg;
   std::vector<std::string> order;
   dit_status st = DIT_OK;
@@ -931,7 +810,7 @@ dit_status dit_profile_end(dit_kernel_stat* stats, int32_t capacity, int32_t* co
     float ms = 0.f;
     hipError_t e = hipEventSynchronize(r.b);
     if (e == hipSuccess) e = hipEventElapsedTime(&ms, r.a, r.b);
-    if (e != hipSuccess && st == DIT_OK) st = fail(DIT_ERR_HIP, "event timing failed: %s", hipGetErrorString(e));
+    if (e != hipSuccess && st == DIT_OK) st = set_error(DIT_ERR_HIP, "event timing failed: %s", hipGetErrorString(e));
     auto it = agg.find(r.name);
     if (it == agg.end()) {
       dit_kernel_stat k{};

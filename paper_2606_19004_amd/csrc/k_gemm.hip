@@ -31,6 +31,7 @@
 //     ordered in groups of 8 M-tiles so concurrently running tiles share A and
 //     W panels in that XCD's L2.
 // fp32 path: VALU tiles (64x64, 4x4 per thread) with the same epilogue.
+#include <atomic>
 #include <type_traits>
 
 #include "internal.h"
@@ -581,14 +582,17 @@ static hipError_t launch_bf16(const GemmPair& pr, hipStream_t s) {
   int total = tiles[0] + tiles[1];
   if (total == 0) return hipSuccess;
   size_t lds = TRI ? (size_t)(2 * BN + 3 * BM) * 64 * 2 : 2 * (size_t)(BM + BN) * 64 * 2;
-  static bool attr_set[64] = {};
+  // The dynamic-LDS limit is raised once per device and kernel instance. Two host threads may reach
+  // this at once; setting the attribute twice is harmless, and the flag is an atomic so the check
+  // itself is race-free.
+  static std::atomic<bool> attr_set[64] = {};
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) dev = 0;
-  if (lds > 65536 && dev < 64 && !attr_set[dev]) {
+  if (lds > 65536 && (dev < 0 || dev >= 64 || !attr_set[dev].load(std::memory_order_acquire))) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_kernel<BM, BN, WM, WN, EPI, OUTF32, MS, TRI>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
-    attr_set[dev] = true;
+    if (dev >= 0 && dev < 64) attr_set[dev].store(true, std::memory_order_release);
   }
   int grid = 8 * cdiv(total, 8);
   gemm_bf16_kernel<BM, BN, WM, WN, EPI, OUTF32, MS, TRI><<<grid, WM * WN * 64, lds, s>>>(pr, tiles[0], total);
@@ -598,15 +602,15 @@ static hipError_t launch_bf16(const GemmPair& pr, hipStream_t s) {
 // Compute units of the current device (one 256 x 256 workgroup fills a CU: 160 KB of LDS and the
 // whole register file), read once per device.
 static int cu_count() {
-  static int cus[64] = {};
+  static std::atomic<int> cus[64] = {};   // 0 = not read yet; concurrent first reads store the same value
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (cus[dev] == 0) {
-    int n = 0;
+  int n = cus[dev].load(std::memory_order_relaxed);
+  if (n == 0) {
     if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
-    cus[dev] = n;
+    cus[dev].store(n, std::memory_order_relaxed);
   }
-  return cus[dev];
+  return n;
 }
 
 template <int EPI, bool OUTF32>

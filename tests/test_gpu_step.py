@@ -142,3 +142,43 @@ def test_step_pieces_full_shape(d):
     d.dit_final_layer(c, d.step_weights(sw), dev(t64.astype(np.float32)), dev(x, "bf16"), v, ws)
     ref_v = O.final_layer(si.as_f64(x, "bf16"), t64.astype(np.float32).astype(np.float64), sw64)
     assert rel_err(v.cpu().numpy(), ref_v) <= 2e-2
+
+
+def _blocks_f64_lazy(inp, cfg):
+    """The blocks' weights as float64, one block at a time (8 blocks at hidden 3072 would take
+    22 GB at once); the oracle walks the stack once."""
+    for b in inp["blocks"]:
+        yield weights_f64(b, cfg.dtype)
+
+
+@pytest.mark.timeout(900)
+def test_step_headline_eight_distinct_blocks_against_oracle(d):
+    """The configuration bench.py times, as it times it: 8 distinct blocks, K=16 seeds, 1024 image +
+    256 text tokens, SDE a=0.7, then the reward statistics of 64 groups x 16 seeds. Two seeds of the
+    step are compared in full with the oracle (velocity and latent delta 2e-2, latent 2e-3); the
+    statistics' order and selection are compared bit for bit."""
+    cfg = si.CONFIGS["step_512_k16"]
+    assert cfg.blocks == 8 and cfg.batch == 16 and cfg.noise_level == 0.7
+    print(f"[headline] generating {cfg.blocks} blocks of seeded weights", flush=True)
+    inp = si.step_inputs(cfg)
+    assert len({id(b) for b in inp["blocks"]}) == 8
+    new, v = run_step(d, cfg, inp)
+    assert np.all(np.isfinite(new)) and np.all(np.isfinite(v))
+    rw = dev(inp["rewards"])
+    G, n, k = cfg.reward_groups, cfg.reward_n, cfg.reward_k
+    outs = [torch.empty(G, device="cuda"), torch.empty(G, device="cuda"), torch.empty((G, n), device="cuda"),
+            torch.empty((G, n), dtype=torch.int32, device="cuda"), torch.empty((G, k), dtype=torch.int32, device="cuda")]
+    d.group_reward_stats(rw, 1e-4, k, *outs)
+    ref_stats = O.group_reward_stats(inp["rewards"].astype(np.float64), 1e-4, k)
+    np.testing.assert_array_equal(outs[3].cpu().numpy(), ref_stats["order"])
+    np.testing.assert_array_equal(outs[4].cpu().numpy(), ref_stats["selected"])
+    seeds = [0, 13]
+    print(f"[headline] oracle for seeds {seeds}", flush=True)
+    sw = {k_: si.as_f64(a, cfg.dtype) for k_, a in inp["step_weights"].items()}
+    lat = inp["latent"][seeds].astype(np.float64)
+    xt = si.as_f64(inp["x_txt"], cfg.dtype)[seeds]
+    eps = inp["eps"][seeds].astype(np.float64)
+    t, tn = float(np.float32(inp["t"])), float(np.float32(inp["t_next"]))
+    ref_new, ref_v, _ = O.denoise_step(cfg, sw, _blocks_f64_lazy(inp, cfg), lat, xt, t, tn, eps,
+                                       float(np.float32(cfg.noise_level)))
+    check_step(cfg, inp, new[seeds], v[seeds], ref_new, ref_v, lat)

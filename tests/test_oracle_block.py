@@ -8,6 +8,7 @@ must have when RoPE is off."""
 import dataclasses
 
 import numpy as np
+import pytest
 import torch
 import torch.nn.functional as F
 
@@ -162,3 +163,49 @@ def test_sampled_rows_equal_full(rng):
     si_, st_ = O.block_forward_sample(CFG, w, temb[1], xi[1], xt[1], img_rows=ri, txt_rows=rt)
     np.testing.assert_allclose(si_, oi[1][ri], rtol=1e-13, atol=1e-14)
     np.testing.assert_allclose(st_, ot[1][rt], rtol=1e-13, atol=1e-14)
+
+
+def _mlp_half_torch(w_s, temb_b, x_b):
+    """The MLP half of one stream for one sample from torch primitives: the modulation chunks are
+    sliced out of F.linear(F.silu(temb)) by position (shift2, scale2, gate2 = chunks 3, 4, 5)."""
+    T = lambda a: torch.from_numpy(np.ascontiguousarray(a))  # noqa: E731
+    d = x_b.shape[-1]
+    m = F.linear(F.silu(T(temb_b)), T(w_s["mod_w"]), T(w_s["mod_b"]))
+    shift2, scale2, gate2 = m[3 * d:4 * d], m[4 * d:5 * d], m[5 * d:6 * d]
+    h2 = F.layer_norm(T(x_b), (d,), eps=1e-6) * (1 + scale2) + shift2
+    u = F.gelu(F.linear(h2, T(w_s["mlp1_w"]), T(w_s["mlp1_b"])), approximate="tanh")
+    return (T(x_b) + gate2 * F.linear(u, T(w_s["mlp2_w"]), T(w_s["mlp2_b"]))).numpy()
+
+
+def _mod_row(w_s, temb_b):
+    return {k: v[0] for k, v in O.modulation(temb_b[None, :], w_s["mod_w"], w_s["mod_b"]).items()}
+
+
+def test_mlp_half_function_against_torch_and_block(rng):
+    """O.mlp_half (the reference of the GPU MLP-half tests) equals a torch composition of the same
+    step, and equals the whole block with gate1 = 0 (only the MLP branch left)."""
+    w = rand_weights(rng)
+    temb, xi, xt = rand_inputs(rng)
+    for s, x in (("img", xi), ("txt", xt)):
+        for b in range(CFG.batch):
+            got = O.mlp_half(w[s], _mod_row(w[s], temb[b]), x[b])
+            np.testing.assert_allclose(got, _mlp_half_torch(w[s], temb[b], x[b]), rtol=1e-11, atol=1e-12)
+    zero_chunk(w, "gate1")
+    oi, ot = O.block_forward(CFG, w, temb, xi, xt)
+    for s, x, out in (("img", xi, oi), ("txt", xt, ot)):
+        for b in range(CFG.batch):
+            np.testing.assert_allclose(O.mlp_half(w[s], _mod_row(w[s], temb[b]), x[b]), out[b],
+                                       rtol=1e-12, atol=1e-13)
+
+
+@pytest.mark.parametrize("swap", [("scale2", "scale1"), ("shift2", "shift1"), ("gate2", "gate1")])
+def test_mlp_half_planted_chunk_mistake_fails_the_pin(rng, swap):
+    """A version of mlp_half that reads the pre-attention chunk instead of the MLP one (e.g. scale1
+    for scale2) is caught by the torch comparison above."""
+    w = rand_weights(rng)
+    temb, xi, _ = rand_inputs(rng)
+    m = _mod_row(w["img"], temb[0])
+    bad = dict(m)
+    bad[swap[0]] = m[swap[1]]
+    ref = _mlp_half_torch(w["img"], temb[0], xi[0])
+    assert not np.allclose(O.mlp_half(w["img"], bad, xi[0]), ref, rtol=1e-11, atol=1e-12)

@@ -112,3 +112,45 @@ def test_planted_mistake_stale_h_prev_changes_distances():
         rels_bad.append(rb)
     assert rels_good[:2] == rels_bad[:2]
     assert rels_good[2] != rels_bad[2]
+
+
+def _block0_input_torch(w0, temb, x_img):
+    """LN(x_img)(1 + scale1) + shift1 from torch primitives, with the image stream's modulation
+    sliced by position (shift1 = chunk 0, scale1 = chunk 1)."""
+    import torch
+    import torch.nn.functional as F
+    T = lambda a: torch.from_numpy(np.ascontiguousarray(a))  # noqa: E731
+    d = x_img.shape[-1]
+    m = F.linear(F.silu(T(temb)), T(w0["img"]["mod_w"]), T(w0["img"]["mod_b"]))
+    shift1, scale1 = m[:, :d], m[:, d:2 * d]
+    return (F.layer_norm(T(x_img), (d,), eps=1e-6) * (1 + scale1[:, None]) + shift1[:, None]).numpy()
+
+
+def _block0_case():
+    rng = np.random.default_rng(77)
+    cfg = si.Shape("pin_b0", hidden=32, heads=2, head_dim=16, grid_h=3, grid_w=4, n_txt=5, batch=3, dtype="f32")
+    w0 = {s: {t: rng.standard_normal(shp) * 0.3 for t, shp in si.block_weight_shapes(cfg).items()}
+          for s in ("img", "txt")}
+    temb = rng.standard_normal((cfg.batch, cfg.hidden))
+    x = rng.standard_normal((cfg.batch, cfg.n_img, cfg.hidden)) * 2.0 + 0.5
+    return w0, temb, x
+
+
+def test_block0_modulated_input_against_torch():
+    w0, temb, x = _block0_case()
+    np.testing.assert_allclose(O.block0_modulated_input(w0, temb, x), _block0_input_torch(w0, temb, x),
+                               rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("mistake", ["chunks_2", "text_stream"])
+def test_block0_modulated_input_planted_mistakes_fail_the_pin(mistake):
+    """Reading the pre-MLP chunks (shift2, scale2) or the text stream's modulation weights instead of
+    the image stream's shift1/scale1 gives a different value, which the torch comparison catches."""
+    w0, temb, x = _block0_case()
+    ref = _block0_input_torch(w0, temb, x)
+    if mistake == "chunks_2":
+        m = O.modulation(temb, w0["img"]["mod_w"], w0["img"]["mod_b"])
+        bad = O.modulate(x, m["shift2"], m["scale2"])
+    else:
+        bad = O.block0_modulated_input({"img": w0["txt"]}, temb, x)
+    assert not np.allclose(bad, ref, rtol=1e-12, atol=1e-12)
