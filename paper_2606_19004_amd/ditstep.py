@@ -146,6 +146,7 @@ def block_weights(img: dict, txt: dict) -> BlockWeights:
     w = BlockWeights()
     for n in _BLOCK_TENSORS:
         setattr(w, n, _P2(_ptr(img.get(n)), _ptr(txt.get(n))))
+    w._keep = (dict(img), dict(txt))   # the struct holds raw device pointers: keep the tensors alive with it
     return w
 
 
@@ -153,6 +154,7 @@ def step_weights(sw: dict) -> StepWeights:
     w = StepWeights()
     for n in _STEP_TENSORS:
         setattr(w, n, _ptr(sw.get(n)))
+    w._keep = dict(sw)
     return w
 
 
