@@ -229,6 +229,20 @@ dit_status dit_timestep_embed(const dit_block_config* cfg, const dit_step_weight
                               const float* t, float* temb, void* workspace, size_t workspace_bytes,
                               dit_stream stream);
 
+/* dit_timestep_embed for callers that cannot allocate (code under HIP graph capture, serving
+ * loops and harnesses that forbid device allocation, callers with no workspace to hand): the
+ * same kernels and result, with their scratch (the sinusoid, the hidden layer and the GEMV's
+ * split input) in a fixed device array the library holds, DIT_TIMESTEP_SCRATCH_BYTES per GPU,
+ * instead of a caller workspace. The call allocates nothing (no hipMalloc, no events).
+ * DIT_ERR_UNSUPPORTED when batch and hidden need more than that array (the need is
+ * batch * (256 + 2 hidden) * 4 bytes plus 64 * hidden bytes, each part rounded up to 256 bytes:
+ * at hidden 3072, up to 156 samples). Every call on a GPU shares that GPU's array: calls that
+ * overlap on one GPU (other streams, other host threads) race and must be serialised by the
+ * caller. Nothing in the array needs to start at zero. */
+#define DIT_TIMESTEP_SCRATCH_BYTES (4u << 20)
+dit_status dit_timestep_embed_noalloc(const dit_block_config* cfg, const dit_step_weights* w, int32_t batch,
+                                      const float* t, float* temb, dit_stream stream);
+
 /* x_img [B][N_i][D] (config dtype) = W_in latent + b_in; latent [B][N_i][C] fp32. */
 dit_status dit_patch_embed(const dit_block_config* cfg, const dit_step_weights* w, int32_t batch,
                            int32_t latent_dim, const float* latent, void* x_img,

@@ -39,9 +39,12 @@ struct Prof {
 };
 Prof g_prof;
 
+// set while an allocation-free entry point runs on this thread: no timing events are created
+thread_local bool g_no_events = false;
+
 template <class F>
 hipError_t timed(const char* name, double flops, double bytes, hipStream_t s, F&& launch) {
-  if (!g_prof.on.load(std::memory_order_acquire)) return launch();
+  if (g_no_events || !g_prof.on.load(std::memory_order_acquire)) return launch();
   hipEvent_t a, b;
   hipError_t e = hipEventCreate(&a);
   if (e != hipSuccess) return e;
@@ -383,6 +386,37 @@ dit_status run_final(const dit_block_config* c, const dit_step_weights* w, int B
   return DIT_OK;
 }
 
+// ---- fixed device scratch of the allocation-free timestep embedding ----
+// The array lives in the library's code object, one copy per GPU it runs on, for the life of the
+// process. Host code never uses its name as an address (on the host it is only a stand-in): the
+// device address comes from hipGetSymbolAddress, taken once per device with that device current.
+constexpr size_t kTimestepScratchBytes = DIT_TIMESTEP_SCRATCH_BYTES;
+}  // namespace
+static __device__ __align__(256) char scratch[DIT_TIMESTEP_SCRATCH_BYTES];
+namespace {
+
+struct ScratchAddrs {
+  std::mutex mu;
+  void* ptr[64] = {};
+};
+ScratchAddrs g_scratch;
+
+dit_status timestep_scratch(void** out) {
+  int dev = -1;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev < 0 || dev >= 64) return set_error(DIT_ERR_UNSUPPORTED, "device %d: at most 64 devices", dev);
+  std::lock_guard<std::mutex> g(g_scratch.mu);
+  if (!g_scratch.ptr[dev]) {
+    void* p = nullptr;
+    hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return set_error(DIT_ERR_HIP, "hipGetSymbolAddress(scratch) failed on device %d: %s", dev, hipGetErrorString(e));
+    g_scratch.ptr[dev] = p;
+  }
+  *out = g_scratch.ptr[dev];
+  return DIT_OK;
+}
+
 }  // namespace
 
 // ===========================================================================
@@ -607,6 +641,25 @@ dit_status dit_timestep_embed(const dit_block_config* c, const dit_step_weights*
   if (!t || !temb) return set_error(DIT_ERR_INVALID_ARG, "t/temb NULL");
   if ((st = check_ws(workspace, workspace_bytes, timestep_ws(c, batch)))) return st;
   return run_timestep(c, w, batch, t, 0.f, temb, (char*)workspace, hs(stream));
+}
+
+dit_status dit_timestep_embed_noalloc(const dit_block_config* c, const dit_step_weights* w, int32_t batch,
+                                      const float* t, float* temb, dit_stream stream) {
+  dit_status st = check_config(c);
+  if (st || (st = check_step_weights(w))) return st;
+  if (batch < 0) return set_error(DIT_ERR_INVALID_ARG, "batch < 0");
+  if (batch == 0) return DIT_OK;
+  if (!t || !temb) return set_error(DIT_ERR_INVALID_ARG, "t/temb NULL");
+  const size_t need = timestep_ws(c, batch);
+  if (need > kTimestepScratchBytes)
+    return set_error(DIT_ERR_UNSUPPORTED, "batch %d at hidden %d needs %zu bytes of scratch, more than the %zu-byte device array",
+                     batch, c->hidden, need, kTimestepScratchBytes);
+  void* ws = nullptr;
+  if ((st = timestep_scratch(&ws))) return st;
+  g_no_events = true;
+  st = run_timestep(c, w, batch, t, 0.f, temb, (char*)ws, hs(stream));
+  g_no_events = false;
+  return st;
 }
 
 dit_status dit_patch_embed(const dit_block_config* c, const dit_step_weights* w, int32_t batch, int32_t latent_dim,
