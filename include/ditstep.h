@@ -17,7 +17,8 @@
  *     caller-provided workspace whose size the *_workspace_bytes() calls give.
  *   - Every call is asynchronous on `stream` (a hipStream_t; NULL = the null
  *     stream), except group_reward_stats, which synchronises `stream` once
- *     to check its small input for NaN.
+ *     to check its small input for NaN (group_reward_stats_async checks on the
+ *     device instead).
  *   - Arguments are validated before any launch; on any error nothing is
  *     written, the status says why and dit_last_error_message() (per host
  *     thread) gives detail. Launch failures return DIT_ERR_HIP.
@@ -218,6 +219,19 @@ dit_status flow_logprob(const float* x, const float* v, const float* x_next, int
 dit_status group_reward_stats(const float* rewards, int32_t groups, int32_t n, float adv_eps,
                               int32_t k_select, float* mean, float* std, float* adv,
                               int32_t* order, int32_t* selected, dit_stream stream);
+
+/* group_reward_stats without the host synchronisation, for callers that keep the stream
+ * asynchronous (a step loop, HIP graph capture): the finiteness check runs on the device. A
+ * one-workgroup pass over the G x n rewards writes *status (device int32) = DIT_OK, or
+ * DIT_ERR_NAN when any reward is NaN or infinite; the statistics kernel then writes its outputs
+ * only when *status is DIT_OK, so on bad input nothing but *status is written. The caller reads
+ * *status after synchronising. Same outputs, bit for bit, as group_reward_stats on finite input.
+ * Arguments are validated on the host as there (DIT_ERR_INVALID_ARG, also for status NULL);
+ * groups == 0 writes nothing, not even *status. */
+dit_status group_reward_stats_async(const float* rewards, int32_t groups, int32_t n, float adv_eps,
+                                    int32_t k_select, float* mean, float* std, float* adv,
+                                    int32_t* order, int32_t* selected, int32_t* status,
+                                    dit_stream stream);
 
 /* ------------------------------------------------------------------ */
 /* full denoise step                                                    */

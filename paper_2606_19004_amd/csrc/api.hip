@@ -628,7 +628,22 @@ dit_status group_reward_stats(const float* rewards, int32_t groups, int32_t n, f
   HIP_TRY(hipStreamSynchronize(s));
   for (size_t i = 0; i < host.size(); i++)
     if (!std::isfinite(host[i])) return set_error(DIT_ERR_NAN, "reward %zu (group %zu) is not finite", i % n, i / n);
-  TIMED("reward_stats", 0, 4.0 * groups * n, s, reward_stats(rewards, groups, n, adv_eps, k_select, mean, stdv, adv, order, selected, s));
+  TIMED("reward_stats", 0, 4.0 * groups * n, s, reward_stats(rewards, groups, n, adv_eps, k_select, mean, stdv, adv, order, selected, nullptr, DIT_ERR_NAN, s));
+  return DIT_OK;
+}
+
+dit_status group_reward_stats_async(const float* rewards, int32_t groups, int32_t n, float adv_eps, int32_t k_select,
+                                    float* mean, float* stdv, float* adv, int32_t* order, int32_t* selected,
+                                    int32_t* status, dit_stream stream) {
+  if (groups < 0) return set_error(DIT_ERR_INVALID_ARG, "groups %d < 0", groups);
+  if (n < 1 || n > 4096) return set_error(DIT_ERR_INVALID_ARG, "n %d outside [1, 4096]", n);
+  if (k_select < 0 || k_select > n) return set_error(DIT_ERR_INVALID_ARG, "k_select %d outside [0, n=%d]", k_select, n);
+  if (!(adv_eps >= 0.f) || !std::isfinite(adv_eps)) return set_error(DIT_ERR_INVALID_ARG, "adv_eps must be >= 0");
+  if (!status) return set_error(DIT_ERR_INVALID_ARG, "status NULL");
+  if (groups == 0) return DIT_OK;
+  if (!rewards) return set_error(DIT_ERR_INVALID_ARG, "rewards NULL");
+  hipStream_t s = hs(stream);
+  TIMED("reward_stats", 0, 4.0 * groups * n, s, reward_stats(rewards, groups, n, adv_eps, k_select, mean, stdv, adv, order, selected, status, DIT_ERR_NAN, s));
   return DIT_OK;
 }
 

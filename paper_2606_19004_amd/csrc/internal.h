@@ -157,8 +157,10 @@ hipError_t teacache_residual(void* x, float* r, int64_t n, int mode, int dtype, 
 constexpr int TEACACHE_PARTS = 512;
 hipError_t flow_update(float* x, const float* v, const float* noise, int64_t n,
                        float cx, float cv, float ce, hipStream_t s);
+// status (device, nullable): a check pass first writes 0 or bad_code (any reward non-finite) there,
+// and the statistics kernel writes nothing when it is non-zero
 hipError_t reward_stats(const float* r, int G, int n, float adv_eps, int k,
                         float* mean, float* stdv, float* adv, int32_t* order, int32_t* sel,
-                        hipStream_t s);
+                        int32_t* status, int32_t bad_code, hipStream_t s);
 
 }  // namespace dit

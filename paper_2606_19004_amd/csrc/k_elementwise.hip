@@ -599,11 +599,25 @@ __device__ double block_sum_f64(double v, double* red) {
   return red[0] + red[1] + red[2] + red[3];
 }
 
+// status[0] = 0 when every one of the `count` rewards is finite, else the non-finite code; one
+// workgroup strides over the input (the reward matrix is small: groups x seeds)
+__global__ void __launch_bounds__(256) reward_check_kernel(const float* __restrict__ rw, int64_t count,
+                                                           int32_t bad_code, int32_t* status) {
+  __shared__ int any[4];
+  int bad = 0;
+  for (int64_t i = threadIdx.x; i < count; i += 256) bad |= !isfinite(rw[i]);
+  bad = __any(bad);
+  if ((threadIdx.x & 63) == 0) any[threadIdx.x >> 6] = bad;
+  __syncthreads();
+  if (threadIdx.x == 0) status[0] = (any[0] | any[1] | any[2] | any[3]) ? bad_code : 0;
+}
+
 __global__ void __launch_bounds__(256) reward_stats_kernel(const float* __restrict__ rw, int n, float adv_eps,
                                                            int k, float* mean, float* stdv, float* adv,
-                                                           int32_t* order, int32_t* sel) {
+                                                           int32_t* order, int32_t* sel, const int32_t* status) {
   extern __shared__ float sr[];               // n rewards, then n ints of order
   __shared__ double red[4];
+  if (status && status[0] != 0) return;       // non-finite input: nothing is written
   int32_t* so = (int32_t*)(sr + n);
   int g = blockIdx.x;
   const float* r = rw + (int64_t)g * n;
@@ -643,10 +657,15 @@ __global__ void __launch_bounds__(256) reward_stats_kernel(const float* __restri
 }
 
 hipError_t reward_stats(const float* r, int G, int n, float adv_eps, int k, float* mean, float* stdv,
-                        float* adv, int32_t* order, int32_t* sel, hipStream_t s) {
+                        float* adv, int32_t* order, int32_t* sel, int32_t* status, int32_t bad_code, hipStream_t s) {
   if (G == 0) return hipSuccess;
+  if (status) {
+    reward_check_kernel<<<1, 256, 0, s>>>(r, (int64_t)G * n, bad_code, status);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   size_t lds = (size_t)n * 8;
-  reward_stats_kernel<<<G, 256, lds, s>>>(r, n, adv_eps, k, mean, stdv, adv, order, sel);
+  reward_stats_kernel<<<G, 256, lds, s>>>(r, n, adv_eps, k, mean, stdv, adv, order, sel, status);
   return hipGetLastError();
 }
 

@@ -27,7 +27,7 @@ STATUS = {0: "DIT_OK", 1: "DIT_ERR_INVALID_ARG", 2: "DIT_ERR_SHAPE", 3: "DIT_ERR
           5: "DIT_ERR_UNSUPPORTED", 6: "DIT_ERR_HIP", 7: "DIT_ERR_WORKSPACE"}
 EXPORTS = ("dit_abi_version", "dit_status_string", "dit_last_error_message", "dit_block_workspace_bytes",
            "dit_block_forward", "dit_block_mlp", "joint_attention", "flow_step", "flow_logprob", "group_reward_stats",
-           "dit_timestep_embed", "dit_timestep_embed_noalloc", "dit_patch_embed", "dit_final_layer", "dit_denoise_workspace_bytes",
+           "group_reward_stats_async", "dit_timestep_embed", "dit_timestep_embed_noalloc", "dit_patch_embed", "dit_final_layer", "dit_denoise_workspace_bytes",
            "dit_denoise_step", "dit_profile_begin", "dit_profile_end", "dit_teacache_init", "dit_teacache_gate",
            "dit_teacache_cache_bytes", "dit_denoise_step_teacache")
 
@@ -83,6 +83,7 @@ _sigs = {
     "flow_step": ([_vp, _vp, _vp, _i64, _f32, _f32, _f32, _stream], _i32),
     "flow_logprob": ([_vp, _vp, _vp, _i32, _i64, _f32, _f32, _f32, _vp, _stream], _i32),
     "group_reward_stats": ([_vp, _i32, _i32, _f32, _i32, _vp, _vp, _vp, _vp, _vp, _stream], _i32),
+    "group_reward_stats_async": ([_vp, _i32, _i32, _f32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _stream], _i32),
     "dit_timestep_embed": ([C.POINTER(BlockConfig), C.POINTER(StepWeights), _i32, _vp, _vp, _vp, _sz, _stream], _i32),
     "dit_timestep_embed_noalloc": ([C.POINTER(BlockConfig), C.POINTER(StepWeights), _i32, _vp, _vp, _stream], _i32),
     "dit_patch_embed": ([C.POINTER(BlockConfig), C.POINTER(StepWeights), _i32, _i32, _vp, _vp, _vp, _sz, _stream], _i32),
@@ -211,6 +212,14 @@ def group_reward_stats(rewards, adv_eps=1e-4, k_select=0, mean=None, std=None, a
     g, n = rewards.shape
     _check(_lib.group_reward_stats(_ptr(rewards), g, n, adv_eps, k_select, _ptr(mean), _ptr(std), _ptr(adv),
                                    _ptr(order), _ptr(selected), _s(stream)))
+
+
+def group_reward_stats_async(rewards, status, adv_eps=1e-4, k_select=0, mean=None, std=None, adv=None, order=None,
+                             selected=None, stream=None):
+    """status: one-element int32 device tensor; holds DIT_OK or DIT_ERR_NAN once the stream has run."""
+    g, n = rewards.shape
+    _check(_lib.group_reward_stats_async(_ptr(rewards), g, n, adv_eps, k_select, _ptr(mean), _ptr(std), _ptr(adv),
+                                         _ptr(order), _ptr(selected), _ptr(status), _s(stream)))
 
 
 def dit_timestep_embed(cfg, sw, t, temb, ws, stream=None):

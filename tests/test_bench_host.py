@@ -129,3 +129,25 @@ def test_stall_summary_fractions_and_conflict_normalisation(tmp_path, monkeypatc
         assert cells[1] == str(n), line
         assert cells[2:8] == ["30.0%", "40.0%", "2.5%", "25.0%", "3.0%", "2.0%"], line
         assert cells[8] == "0.1000", line
+
+
+def test_kernel_entry_classifies_by_arithmetic_intensity():
+    import bench
+    # modulation GEMV of the step: 16 samples -> 16 flop per weight byte, far below the ridge point
+    gemv = bench.kernel_entry({"name": "mod_gemv", "launches": 1, "total_ms": 0.5,
+                               "flops": 2.0 * 16 * 16 * 18432 * 3072, "bytes": 16 * 18432 * 3072 * 2.0})
+    assert gemv["bound"] == "hbm"
+    assert gemv["gbs"] == round(16 * 18432 * 3072 * 2.0 / 0.5e-3 / 1e9, 1)
+    assert gemv["frac_hbm"] == round(gemv["gbs"] / bench.PEAK_HBM_GBS, 4)
+    assert "frac_mfma" in gemv   # flops are still reported
+    # a GEMM class carries no byte count: MFMA-bound
+    gemm = bench.kernel_entry({"name": "gemm_mlp_up_gelu", "launches": 8, "total_ms": 9.5,
+                               "flops": 8 * 1.546e12, "bytes": 0})
+    assert gemm["bound"] == "mfma" and "gbs" not in gemm
+    assert gemm["frac_mfma"] == round(round(8 * 1.546e12 / 9.5e-3 / 1e12, 1) / bench.PEAK_BF16_TFLOPS, 4)
+    # byte-only classes (LayerNorm, flow update) are HBM-bound
+    ln = bench.kernel_entry({"name": "ln_modulate", "launches": 2, "total_ms": 0.12, "flops": 0, "bytes": 5.0e8})
+    assert ln["bound"] == "hbm" and "tflops" not in ln
+    # above the ridge point a class with bytes is MFMA-bound
+    dense = bench.kernel_entry({"name": "x", "launches": 1, "total_ms": 1.0, "flops": 1e12, "bytes": 1e9})
+    assert dense["bound"] == "mfma" and "gbs" not in dense

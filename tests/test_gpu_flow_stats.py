@@ -114,6 +114,40 @@ def test_reward_stats_constant_and_errors(d):
     assert ei.value.name == "DIT_ERR_INVALID_ARG"
 
 
+def test_reward_stats_async_matches_sync_and_flags_bad_input(d):
+    # the device-checked variant: same outputs bit for bit on finite input, status DIT_OK; on a
+    # NaN or Inf reward status DIT_ERR_NAN and every output left as it was
+    rng = np.random.default_rng(5)
+    for g, n, k in ((64, 16, 4), (3, 4096, 7), (1, 1, 1)):
+        r = rng.uniform(size=(g, n)).astype(np.float32)
+        r[:, : n // 3] = r[:, :1]   # ties
+        want = _stats(d, r, k)
+        outs = {"mean": torch.full((g,), -1.0, device="cuda"), "std": torch.full((g,), -1.0, device="cuda"),
+                "adv": torch.full((g, n), -1.0, device="cuda"),
+                "order": torch.full((g, n), -1, dtype=torch.int32, device="cuda"),
+                "selected": torch.full((g, max(k, 1)), -1, dtype=torch.int32, device="cuda")}
+        status = torch.full((1,), -1, dtype=torch.int32, device="cuda")
+        d.group_reward_stats_async(dev(r), status, 1e-4, k, **outs)
+        torch.cuda.synchronize()
+        assert int(status.item()) == 0
+        for key in ("mean", "std", "adv", "order"):
+            np.testing.assert_array_equal(outs[key].cpu().numpy(), want[key], err_msg=key)
+        np.testing.assert_array_equal(outs["selected"].cpu().numpy()[:, :k], want["selected"])
+    for bad_value in (np.nan, np.inf, -np.inf):
+        bad = rng.uniform(size=(5, 32)).astype(np.float32)
+        bad[4, 31] = bad_value
+        mean = torch.full((5,), -7.0, device="cuda")
+        order = torch.full((5, 32), -3, dtype=torch.int32, device="cuda")
+        status = torch.zeros((1,), dtype=torch.int32, device="cuda")
+        d.group_reward_stats_async(dev(bad), status, 1e-4, 2, mean=mean, order=order)
+        torch.cuda.synchronize()
+        assert int(status.item()) == 4   # DIT_ERR_NAN
+        assert torch.all(mean == -7.0) and torch.all(order == -3)
+    with pytest.raises(d.DitError) as ei:
+        d.group_reward_stats_async(dev(np.zeros((2, 4), np.float32)), None, 1e-4, 1)
+    assert ei.value.name == "DIT_ERR_INVALID_ARG"
+
+
 # ----------------------------------------------------------------------------------------------
 # flow_logprob: the log-density of an SDE step's output under its Gaussian transition
 # ----------------------------------------------------------------------------------------------
