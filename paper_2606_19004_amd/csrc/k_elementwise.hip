@@ -480,11 +480,14 @@ __global__ void split_hilo_kernel(const float* __restrict__ in, int64_t stride, 
 
 // One workgroup = 16 RB weight rows (RB row blocks of 16, each the A operand of its own MFMA
 // chain); its 4 waves take every 4th 32-deep k step and the partial sums meet in LDS, so each
-// row block streams with 4 independent load chains. More row blocks per workgroup means fewer
-// re-reads of the split input per weight byte (RB = 4 measured 7% faster than 2; 8 slower).
-constexpr int GEMV_RB = 4;
+// row block streams with 4 independent load chains. Every k step of a wave reads the split input
+// (2 x 1 KB from L2) once for its RB row blocks (RB x 1 KB of weights), so more row blocks per
+// workgroup mean fewer re-reads of the input per weight byte: with the weights cold in HBM, RB = 8
+// (one k step per wave in flight, 180 registers) streams the 1.81 GB of a step's modulation
+// weights in 426 us against 467 us for RB = 4 with two k steps in flight. Small GEMVs (the
+// timestep and final-layer ones) keep RB = 4, which gives twice the workgroups to fill the chip.
+template <int RB, int U>
 __global__ void __launch_bounds__(256) gemv_mfma_kernel(GemvArgs a, const u16* __restrict__ xs, int b0, int nb) {
-  constexpr int RB = GEMV_RB, U = 2;
   __shared__ f32x4 part[4][RB][64];
   const int s = blockIdx.y;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -563,7 +566,10 @@ hipError_t gemv_bf16(const GemvArgs& a, u16* xs, int silu_in, hipStream_t s) {
   for (int b0 = 0; b0 < a.B; b0 += 16) {
     int nb = std::min(16, a.B - b0);
     split_hilo_kernel<<<dim3(cdiv(a.K, 256), 16), 256, 0, s>>>(a.in, a.in_bstride, b0, nb, a.K, silu_in, xs);
-    gemv_mfma_kernel<<<dim3(cdiv(a.N, 16 * GEMV_RB), a.nstreams), 256, 0, s>>>(a, xs, b0, nb);
+    if ((int64_t)cdiv(a.N, 128) * a.nstreams >= 1024)
+      gemv_mfma_kernel<8, 1><<<dim3(cdiv(a.N, 128), a.nstreams), 256, 0, s>>>(a, xs, b0, nb);
+    else
+      gemv_mfma_kernel<4, 2><<<dim3(cdiv(a.N, 64), a.nstreams), 256, 0, s>>>(a, xs, b0, nb);
   }
   return hipGetLastError();
 }

@@ -8,7 +8,11 @@
 //     need (RoPE pairs (2i, 2i+1) sit in one lane).
 //   * Tiles of A and W move HBM -> LDS with buffer_load ... lds (no VGPR
 //     staging). Out-of-range rows use an offset past the buffer's num_records,
-//     which the hardware turns into zeros.
+//     which the hardware turns into zeros. In the large tile a wave's refill of
+//     one operand is a single burst of up to four such loads under one M0 value
+//     (the instruction offset steps the LDS destination by 1 KB): a load issued
+//     between MFMAs holds the wave's issue for ~17 cycles, and the M0 save and
+//     restore around each load for ~13 more, while back-to-back loads share it.
 //   * LDS rows are 64 bf16 = 8 chunks of 16 bytes; chunk c of row r is stored
 //     at slot c ^ ((r >> 1) & 7), so every lane group that a ds_read_b128 of a
 //     fragment is served in hits 16 different bank groups of the 64-bank LDS.
@@ -129,6 +133,28 @@ __device__ __forceinline__ void dma_b128(u32x4_t rsrc, uint32_t m0v, uint32_t vo
                : "=&s"(saved) : "s"(m0v), "v"(voff), "s"(rsrc), "s"(soff) : "memory");
 }
 
+// N (3 or 4) direct-to-LDS loads sharing one M0: destination M0 + 1024 i + 16 lane, global offset
+// v[i] + 1024 i (the instruction offset moves both addresses)
+template <int N>
+__device__ __forceinline__ void dma_burst(u32x4_t rsrc, uint32_t m0v, const uint32_t* v, uint32_t soff) {
+  uint32_t saved;
+  if constexpr (N == 4)
+    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\t"
+                 "buffer_load_dwordx4 %2, %6, %7 offen lds\n\t"
+                 "buffer_load_dwordx4 %3, %6, %7 offen offset:1024 lds\n\t"
+                 "buffer_load_dwordx4 %4, %6, %7 offen offset:2048 lds\n\t"
+                 "buffer_load_dwordx4 %5, %6, %7 offen offset:3072 lds\n\t"
+                 "s_mov_b32 m0, %0"
+                 : "=&s"(saved) : "s"(m0v), "v"(v[0]), "v"(v[1]), "v"(v[2]), "v"(v[3]), "s"(rsrc), "s"(soff) : "memory");
+  else
+    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\t"
+                 "buffer_load_dwordx4 %2, %5, %6 offen lds\n\t"
+                 "buffer_load_dwordx4 %3, %5, %6 offen offset:1024 lds\n\t"
+                 "buffer_load_dwordx4 %4, %5, %6 offen offset:2048 lds\n\t"
+                 "s_mov_b32 m0, %0"
+                 : "=&s"(saved) : "s"(m0v), "v"(v[0]), "v"(v[1]), "v"(v[2]), "s"(rsrc), "s"(soff) : "memory");
+}
+
 __device__ __forceinline__ void tile_coords(int tl, int mt, int nt, int& tm, int& tn) {
   constexpr int GROUP_M = 8;
   int per_group = GROUP_M * nt;
@@ -247,20 +273,32 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_bf16_kernel(GemmPair pr, in
   auto stage_a = [&](int kt) -> char* { return smem + 2 * W_BYTES + (kt % 3) * A_BYTES; };
   const int wave_s = __builtin_amdgcn_readfirstlane(wave);
   const uint64_t pa64 = (uint64_t)P.A, pw64 = (uint64_t)P.W;
-  const u32x4_t ra4 = {(uint32_t)pa64, (uint32_t)(pa64 >> 32) & 0xffffu, 0x7fffffffu, 0x00020000u};
-  const u32x4_t rw4 = {(uint32_t)pw64, (uint32_t)(pw64 >> 32) & 0xffffu, 0x7fffffffu, 0x00020000u};
+  // refills as one burst per operand: offsets carry -1024 i plus a 4 KB bias taken back from the base
+  constexpr bool BA = TRI && (A_LOADS == 3 || A_LOADS == 4), BW = TRI && (W_LOADS == 3 || W_LOADS == 4);
+  const uint64_t pa64b = pa64 - (BA ? 4096u : 0u), pw64b = pw64 - (BW ? 4096u : 0u);
+  // (with the bias every in-range offset stays below 2^31 + 4 KB, the records bound; rows outside the
+  // matrix move to 3 GiB, past it, and still read zeros)
+  const u32x4_t ra4 = {(uint32_t)pa64b, (uint32_t)(pa64b >> 32) & 0xffffu, BA ? 0x80001000u : 0x7fffffffu, 0x00020000u};
+  const u32x4_t rw4 = {(uint32_t)pw64b, (uint32_t)(pw64b >> 32) & 0xffffu, BW ? 0x80001000u : 0x7fffffffu, 0x00020000u};
+  uint32_t aoffb[A_LOADS], woffb[W_LOADS];
+#pragma unroll
+  for (int i = 0; i < A_LOADS; i++) aoffb[i] = BA ? (aoff[i] == OOB ? 0xC0000000u : aoff[i]) + 4096u - 1024u * i : aoff[i];
+#pragma unroll
+  for (int i = 0; i < W_LOADS; i++) woffb[i] = BW ? (woff[i] == OOB ? 0xC0000000u : woff[i]) + 4096u - 1024u * i : woff[i];
   const uint32_t smem_lds = (uint32_t)(uintptr_t)(lds_ptr_t)smem;
   auto issue_a = [&](int kt) {
     const uint32_t sa = smem_lds + (uint32_t)(stage_a(kt) - smem);
     const uint32_t soff = kt * BK * 2;
 #pragma unroll
-    for (int i = 0; i < A_LOADS; i++) dma_b128(ra4, sa + (wave_s * A_LOADS + i) * 1024, aoff[i], soff);
+    for (int i = 0; i < (BA ? 0 : A_LOADS); i++) dma_b128(ra4, sa + (wave_s * A_LOADS + i) * 1024, aoffb[i], soff);
+    if constexpr (BA) dma_burst<A_LOADS>(ra4, sa + wave_s * A_LOADS * 1024, aoffb, soff);
   };
   auto issue_w = [&](int kt) {
     const uint32_t sw = smem_lds + (uint32_t)(stage_w(kt) - smem);
     const uint32_t soff = kt * BK * 2;
 #pragma unroll
-    for (int i = 0; i < W_LOADS; i++) dma_b128(rw4, sw + (wave_s * W_LOADS + i) * 1024, woff[i], soff);
+    for (int i = 0; i < (BW ? 0 : W_LOADS); i++) dma_b128(rw4, sw + (wave_s * W_LOADS + i) * 1024, woffb[i], soff);
+    if constexpr (BW) dma_burst<W_LOADS>(rw4, sw + wave_s * W_LOADS * 1024, woffb, soff);
   };
   auto issue = [&](int kt, int buf) {
     char* sa = smem + buf * (A_BYTES + W_BYTES);
