@@ -40,7 +40,8 @@ STALL_COUNTERS = ("SQ_WAVE_CYCLES", "SQ_WAIT_ANY", "SQ_WAIT_INST_ANY", "SQ_WAIT_
                   "SQ_ACTIVE_INST_LDS", "SQ_LDS_BANK_CONFLICT", "SQ_INST_CYCLES_VMEM_RD", "GRBM_GUI_ACTIVE")
 # source file whose kernels each counted class runs (a summary is stale once that file changes)
 CLASS_SOURCE = {"gemm_qkv_rope": "k_gemm.hip", "gemm_out_gate": "k_gemm.hip", "gemm_mlp_up_gelu": "k_gemm.hip",
-                "gemm_mlp_down_gate": "k_gemm.hip", "attention": "k_attn.hip", "ln_modulate": "k_elementwise.hip"}
+                "gemm_mlp_down_gate": "k_gemm.hip", "attention": "k_attn.hip", "ln_modulate": "k_elementwise.hip",
+                "mod_gemv": "k_elementwise.hip"}
 
 
 def parse():
@@ -134,6 +135,8 @@ def classify_dispatches(rows):
             cls = "attention"
         elif "ln_modulate_kernel" in n:
             cls = "ln_modulate"
+        elif "gemv_mfma_kernel<8" in n:   # only the batched modulation GEMV is large enough for 8 row blocks
+            cls = "mod_gemv"
         prev = cur
         out.append(cls)
     return out
@@ -350,7 +353,9 @@ def traffic_summary(run_dir, cfg):
             "gemm_mlp_up_gelu": 2 * (M * D + F * D + M * F),
             "gemm_mlp_down_gate": 2 * (M * F + D * F + 2 * M * D),
             "attention": 2 * 4 * M * D,
-            "ln_modulate": 2 * 2 * M * D}
+            "ln_modulate": 2 * 2 * M * D,
+            # modulation of up to 8 blocks x 2 streams: [6D][D] bf16 weights read, [B][6D] fp32 written
+            "mod_gemv": 2 * min(8, cfg.blocks) * (6 * D * D * 2 + cfg.batch * 6 * D * 4)}
     classes = {}
     for cls, v in per.items():
         fk = sum(v["FETCH_SIZE"]) / len(v["FETCH_SIZE"])
