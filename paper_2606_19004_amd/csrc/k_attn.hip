@@ -6,7 +6,8 @@
 //   * K and V tiles go from global memory straight into LDS (buffer loads with the
 //     LDS-destination bit), double-buffered: tile t+1 streams in while tile t is
 //     multiplied. The buffer resource spans exactly this (sample, head)'s rows, so
-//     keys past the end read as zeros with no bounds arithmetic.
+//     keys past the end read as zeros with no bounds arithmetic. With head_dim 128 a
+//     wave's four loads per operand go out as one burst under a single M0 value.
 //   * Scores are computed transposed, S^T = K Q^T, with v_mfma_f32_32x32x16_bf16:
 //     operand A = 32 keys (K rows from LDS), operand B = 32 queries (Q rows held
 //     in registers for the whole loop). Each lane then owns ONE query column
@@ -56,6 +57,25 @@ __device__ __forceinline__ float pair_sum(float v) {
   float a, b;
   half_pair(v, a, b);
   return a + b;
+}
+
+typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+
+// Four direct-to-LDS loads under one M0 value: destination M0 + 1024 i + 16 lane, global offset
+// v[i] + 1024 i (the instruction offset moves both addresses). Issued back to back they hold the
+// wave's issue for less than four separately issued loads, each of which sets M0 on its own.
+// Inline assembly, so the compiler does not track these loads: the wait before the barrier that
+// hands a stage over is the explicit s_waitcnt(0) of the loop.
+__device__ __forceinline__ void dma4_b128(u32x4_t rsrc, uint32_t m0v, uint32_t v0, uint32_t v1, uint32_t v2,
+                                          uint32_t v3) {
+  uint32_t saved;
+  asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\t"
+               "buffer_load_dwordx4 %2, %6, 0 offen lds\n\t"
+               "buffer_load_dwordx4 %3, %6, 0 offen offset:1024 lds\n\t"
+               "buffer_load_dwordx4 %4, %6, 0 offen offset:2048 lds\n\t"
+               "buffer_load_dwordx4 %5, %6, 0 offen offset:3072 lds\n\t"
+               "s_mov_b32 m0, %0"
+               : "=&s"(saved) : "s"(m0v), "v"(v0), "v"(v1), "v"(v2), "v"(v3), "s"(rsrc) : "memory");
 }
 
 template <int D>
@@ -112,8 +132,22 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_bf16(AttnArgs a) {
     koff[i] = row * rowstride + ((slot ^ (row % CH)) << 4);
     voff[i] = row * rowstride + ((slot ^ ((row & 3) * (CH / 4))) << 4);
   }
+  // head_dim 128: a wave's share of a K (or V) tile is four consecutive 1 KB blocks, loaded as one burst.
+  // Those descriptors start 4 KB early (and span 4 KB more) so that no per-lane offset goes negative.
+  const uint64_t k64 = (uint64_t)Kg - 4096, v64 = (uint64_t)Vg - 4096;
+  const u32x4_t rk4 = {(uint32_t)k64, (uint32_t)(k64 >> 32) & 0xffffu, nrec + 4096u, 0x00020000u};
+  const u32x4_t rv4 = {(uint32_t)v64, (uint32_t)(v64 >> 32) & 0xffffu, nrec + 4096u, 0x00020000u};
+  const uint32_t wdst = (uint32_t)(__builtin_amdgcn_readfirstlane(wave) * LOADS * KPI * RB);
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_ptr_t)smem;
   auto issue = [&](int kt, int buf) {
     const uint32_t base = (uint32_t)(kt * KB) * rowstride;
+    if constexpr (LOADS == 4) {
+      dma4_b128(rk4, lds0 + buf * TILE + wdst, base + koff[0] + 4096u, base + koff[1] + 3072u, base + koff[2] + 2048u,
+                base + koff[3] + 1024u);
+      dma4_b128(rv4, lds0 + (2 + buf) * TILE + wdst, base + voff[0] + 4096u, base + voff[1] + 3072u,
+                base + voff[2] + 2048u, base + voff[3] + 1024u);
+      return;
+    }
 #pragma unroll
     for (int i = 0; i < LOADS; i++) {
       const int dst = (wave * LOADS + i) * KPI * RB;
