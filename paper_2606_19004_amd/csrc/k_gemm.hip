@@ -155,6 +155,13 @@ __device__ __forceinline__ void dma_burst(u32x4_t rsrc, uint32_t m0v, const uint
                  : "=&s"(saved) : "s"(m0v), "v"(v[0]), "v"(v[1]), "v"(v[2]), "s"(rsrc), "s"(soff) : "memory");
 }
 
+// Exchange lanes 16-31 of x with lanes 0-15 of y and lanes 48-63 of x with lanes 32-47 of y.
+__device__ __forceinline__ void swap16(uint32_t& x, uint32_t& y) {
+  const auto r = __builtin_amdgcn_permlane16_swap(x, y, false, false);
+  x = r[0];
+  y = r[1];
+}
+
 __device__ __forceinline__ void tile_coords(int tl, int mt, int nt, int& tm, int& tn) {
   constexpr int GROUP_M = 8;
   int per_group = GROUP_M * nt;
@@ -489,26 +496,60 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_bf16_kernel(GemmPair pr, in
   //   MS = 32: n = 32 i + 8 g + 4 (lane / 32) + q, m = 32 j + lane % 32
   //   MS = 16: n = 16 i + 4 (lane / 16) + q,        m = 16 j + lane % 16
   constexpr int NG = NACC / 4;
-  // MS = 16: the residual values of this wave's whole sub-tile (one 4-column group per block (i, j),
-  // 64 registers, free now that the fragment registers are dead) are requested at once, before the
-  // staging barriers, so their memory latency is paid once per tile and overlaps the staging
+  // MS = 16 with bf16 output: blocks i and i + 1 of a row group (32 adjacent columns) are finished
+  // together and regrouped with v_permlane16_swap, which exchanges lanes 16-31 of one register with
+  // lanes 0-15 of another (and 48-63 with 32-47). Lane group g = lane / 16 then holds the 8 adjacent
+  // columns 32 p + 16 (g & 1) + 8 (g >> 1) of pair p, stored with one 16-byte store. A CU issues a
+  // store of 16 rows x 32 B (the accumulator layout) in ~74 cycles and one of 16 rows x 64 B in ~20,
+  // and with 256 stores per tile that issue time, not HBM, bounded the epilogue. The paired layout
+  // needs 16-byte aligned output rows; otherwise the accumulator layout is stored as it is.
+  constexpr bool PAIRS = MS == 16 && !OUTF32;
+  static_assert(!PAIRS || TI % 2 == 0, "the paired store joins blocks 2p and 2p + 1");
+  const bool pairs = PAIRS && (P.N & 7) == 0 && ((uintptr_t)P.C & 15) == 0 &&
+                     ((P.cmap.batch_stride | P.cmap.row_stride | P.cmap.offset) & 7) == 0;
+  const int pair_col = 16 * (lkc & 1) + 8 * (lkc >> 1);
+  // MS = 16: the residual values of this wave's whole sub-tile (64 registers, free now that the
+  // fragment registers are dead) are requested at once, before the staging barriers, so their memory
+  // latency is paid once per tile and overlaps the staging. xq[j][p] holds blocks (2p, j) and
+  // (2p + 1, j): in the paired layout as loaded (one 16-byte load), else as two 8-byte loads in the
+  // accumulator layout.
   constexpr bool XALL = EPI == EPI_RESID && MS == 16;
-  uint2 xall[XALL ? TJ : 1][XALL ? TI : 1];
+  static_assert(!XALL || PAIRS, "the residual preload assumes paired blocks");
+  uint4 xq[XALL ? TJ : 1][XALL ? TI / 2 : 1];
   if constexpr (XALL) {
     // buffer loads, so that no load sits in a branch: a conditional load leaves the compiler unable to
     // count the loads in flight, and it then waits for every earlier memory operation (stores
     // included) before each use
     const uint32_t OOB = 0x80000000u;
     const __amdgpu_buffer_rsrc_t rc = __builtin_amdgcn_make_buffer_rsrc(P.C, (short)0, 0x7fffffff, 0x00020000);
+    if (pairs) {
 #pragma unroll
-    for (int j = 0; j < TJ; j++) {
-      const int m = m0 + wm * WTM + MS * j + frow;
-      const uint32_t roff = m < P.M ? (uint32_t)(row_epi(P, m).off * 2) : OOB;
+      for (int j = 0; j < TJ; j++) {
+        const int m = m0 + wm * WTM + MS * j + frow;
+        const uint32_t roff = m < P.M ? (uint32_t)(row_epi(P, m).off * 2) : OOB;
 #pragma unroll
-      for (int i = 0; i < TI; i++) {
-        const int n = n0 + wn * WTN + MS * i + 4 * lkc;
-        const uint32_t off = (m < P.M && n < P.N) ? roff + (uint32_t)n * 2u : OOB;
-        xall[j][i] = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rc, off, 0, 0));
+        for (int p = 0; p < TI / 2; p++) {
+          const int c = n0 + wn * WTN + 32 * p + pair_col;
+          const uint32_t off = (m < P.M && c < P.N) ? roff + (uint32_t)c * 2u : OOB;
+          xq[j][p] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rc, off, 0, 0));
+        }
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < TJ; j++) {
+        const int m = m0 + wm * WTM + MS * j + frow;
+        const uint32_t roff = m < P.M ? (uint32_t)(row_epi(P, m).off * 2) : OOB;
+#pragma unroll
+        for (int p = 0; p < TI / 2; p++) {
+          uint2 h[2];
+#pragma unroll
+          for (int e = 0; e < 2; e++) {
+            const int n = n0 + wn * WTN + MS * (2 * p + e) + 4 * lkc;
+            const uint32_t off = (m < P.M && n < P.N) ? roff + (uint32_t)n * 2u : OOB;
+            h[e] = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rc, off, 0, 0));
+          }
+          xq[j][p] = make_uint4(h[0].x, h[0].y, h[1].x, h[1].y);
+        }
       }
     }
   }
@@ -578,7 +619,11 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_bf16_kernel(GemmPair pr, in
           }
           if (EPI == EPI_RESID) {
             float4 gv = STAGED ? *(const float4*)(s_gate + bt * BN + nl) : *(const float4*)(P.gate + R.gate + n);
-            uint2 u = XALL ? xall[XALL ? j : 0][XALL ? i : 0] : xr[i & 1][g];
+            uint2 u = xr[i & 1][g];
+            if constexpr (XALL) {
+              const uint4 q = xq[j][i >> 1];
+              u = (i & 1) ? make_uint2(q.z, q.w) : make_uint2(q.x, q.y);
+            }
             v[0] = fmaf(gv.x, v[0], __uint_as_float(u.x << 16));
             v[1] = fmaf(gv.y, v[1], __uint_as_float(u.x & 0xffff0000u));
             v[2] = fmaf(gv.z, v[2], __uint_as_float(u.y << 16));
@@ -603,12 +648,84 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_bf16_kernel(GemmPair pr, in
       }
     }
   };
+  // The paired store: the same arithmetic per accumulator block as store_tile, then the regrouping
+  // swap on the packed bf16 pairs and one 16-byte store per pair of blocks. The residual values arrive
+  // in the paired layout and go through the same swap (it is its own inverse) before use.
+  auto store_pairs = [&](auto staged_c) {
+    constexpr bool STAGED = decltype(staged_c)::value;
+    if constexpr (PAIRS) {
+#pragma unroll
+      for (int j = 0; j < TJ; j++) {
+        const int m = m0 + wm * WTM + MS * j + frow;
+        if (m >= P.M) continue;   // the swap partners (lanes l and l ^ 16) share the row m
+        const RowEpi R = row_epi(P, m);
+        const int bt = m / rpb - bfirst;
+#pragma unroll
+        for (int p = 0; p < TI / 2; p++) {
+          uint4 xr = make_uint4(0u, 0u, 0u, 0u);
+          if constexpr (XALL) {
+            xr = xq[j][p];
+            swap16(xr.x, xr.z);
+            swap16(xr.y, xr.w);
+          }
+          uint32_t w[2][2];
+#pragma unroll
+          for (int e = 0; e < 2; e++) {
+            const int i = 2 * p + e;
+            const int nl = wn * WTN + MS * i + 4 * lkc;   // column inside the tile
+            const int n = n0 + nl;
+            float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+            float4 bv = *(const float4*)(s_bias + nl);
+            v[0] += bv.x; v[1] += bv.y; v[2] += bv.z; v[3] += bv.w;
+            if (EPI == EPI_GELU) {
+#pragma unroll
+              for (int q = 0; q < 4; q++) v[q] = gelu_tanh_f(v[q]);
+            }
+            if (EPI == EPI_RESID) {
+              float4 gv = make_float4(0.f, 0.f, 0.f, 0.f);
+              if (STAGED) gv = *(const float4*)(s_gate + bt * BN + nl);
+              else if (n < P.N) gv = *(const float4*)(P.gate + R.gate + n);
+              const uint32_t u0 = e ? xr.z : xr.x, u1 = e ? xr.w : xr.y;
+              v[0] = fmaf(gv.x, v[0], __uint_as_float(u0 << 16));
+              v[1] = fmaf(gv.y, v[1], __uint_as_float(u0 & 0xffff0000u));
+              v[2] = fmaf(gv.z, v[2], __uint_as_float(u1 << 16));
+              v[3] = fmaf(gv.w, v[3], __uint_as_float(u1 & 0xffff0000u));
+            }
+            if (EPI == EPI_QKV && rope_on && n < rope_cols) {
+              int dd = n & (head_dim - 1);
+              int hh = head_dim >> 1;
+              int pos = dd < hh ? R.rpos : R.cpos;
+              int pr = (dd & (hh - 1)) >> 1;
+              int ti = (pos * (head_dim >> 2) + pr) * 2;
+              float4 t = STAGED ? *(const float4*)(s_rope + ti) : *(const float4*)(P.rope_tab + ti);
+              float a0 = v[0], b0 = v[1], a1 = v[2], b1 = v[3];
+              v[0] = a0 * t.x - b0 * t.y;
+              v[1] = a0 * t.y + b0 * t.x;
+              v[2] = a1 * t.z - b1 * t.w;
+              v[3] = a1 * t.w + b1 * t.z;
+            }
+            w[e][0] = pack_bf16x2(v[0], v[1]);
+            w[e][1] = pack_bf16x2(v[2], v[3]);
+          }
+          swap16(w[0][0], w[1][0]);
+          swap16(w[0][1], w[1][1]);
+          const int c = n0 + wn * WTN + 32 * p + pair_col;
+          if (c < P.N) *(uint4*)((u16*)P.C + R.off + c) = make_uint4(w[0][0], w[0][1], w[1][0], w[1][1]);
+        }
+      }
+    }
+  };
   const bool staged = (EPI != EPI_RESID || gate_lds) && (!rope_on || rope_lds);
   // XALL: every residual load has landed before the first store. The compiler cannot order stores
   // against loads on this counter, so inside the loop it would instead wait for earlier stores.
   if constexpr (XALL) __builtin_amdgcn_s_waitcnt(0);
-  if (staged) store_tile(std::true_type());
-  else store_tile(std::false_type());
+  if (pairs) {
+    if (staged) store_pairs(std::true_type());
+    else store_pairs(std::false_type());
+  } else {
+    if (staged) store_tile(std::true_type());
+    else store_tile(std::false_type());
+  }
 #endif
 }
 
