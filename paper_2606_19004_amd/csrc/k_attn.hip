@@ -4,10 +4,14 @@
 // queries of one (sample, head); K/V tiles of 64 keys staged in LDS and shared
 // by the 4 waves; online softmax in the exp2 domain with fp32 statistics.
 //   * K and V tiles go from global memory straight into LDS (buffer loads with the
-//     LDS-destination bit), double-buffered: tile t+1 streams in while tile t is
-//     multiplied. The buffer resource spans exactly this (sample, head)'s rows, so
-//     keys past the end read as zeros with no bounds arithmetic. With head_dim 128 a
-//     wave's four loads per operand go out as one burst under a single M0 value.
+//     LDS-destination bit), two LDS buffers each. The buffer resource spans exactly
+//     this (sample, head)'s rows, so keys past the end read as zeros with no bounds
+//     arithmetic. With head_dim 128 a wave's four loads per operand go out as one
+//     burst under a single M0 value.
+//   * Software pipeline: the step for tile t takes the exponentials of tile t and the
+//     score MFMAs of tile t+1 in one instruction stream (neither depends on the
+//     other, so the MFMAs issue between the VALU work), then tile t's P V^T. K tiles
+//     are therefore requested two tiles ahead and V tiles one ahead.
 //   * Scores are computed transposed, S^T = K Q^T, with v_mfma_f32_32x32x16_bf16:
 //     operand A = 32 keys (K rows from LDS), operand B = 32 queries (Q rows held
 //     in registers for the whole loop). Each lane then owns ONE query column
@@ -139,21 +143,31 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_bf16(AttnArgs a) {
   const u32x4_t rv4 = {(uint32_t)v64, (uint32_t)(v64 >> 32) & 0xffffu, nrec + 4096u, 0x00020000u};
   const uint32_t wdst = (uint32_t)(__builtin_amdgcn_readfirstlane(wave) * LOADS * KPI * RB);
   const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_ptr_t)smem;
-  auto issue = [&](int kt, int buf) {
+  auto issue_k = [&](int kt, int buf) {
     const uint32_t base = (uint32_t)(kt * KB) * rowstride;
     if constexpr (LOADS == 4) {
       dma4_b128(rk4, lds0 + buf * TILE + wdst, base + koff[0] + 4096u, base + koff[1] + 3072u, base + koff[2] + 2048u,
                 base + koff[3] + 1024u);
+    } else {
+#pragma unroll
+      for (int i = 0; i < LOADS; i++) {
+        const int dst = (wave * LOADS + i) * KPI * RB;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_ptr_t)(smem + buf * TILE + dst), 16, base + koff[i], 0, 0, 0);
+      }
+    }
+  };
+  auto issue_v = [&](int kt, int buf) {
+    const uint32_t base = (uint32_t)(kt * KB) * rowstride;
+    if constexpr (LOADS == 4) {
       dma4_b128(rv4, lds0 + (2 + buf) * TILE + wdst, base + voff[0] + 4096u, base + voff[1] + 3072u,
                 base + voff[2] + 2048u, base + voff[3] + 1024u);
-      return;
-    }
+    } else {
 #pragma unroll
-    for (int i = 0; i < LOADS; i++) {
-      const int dst = (wave * LOADS + i) * KPI * RB;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_ptr_t)(smem + buf * TILE + dst), 16, base + koff[i], 0, 0, 0);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_ptr_t)(smem + (2 + buf) * TILE + dst), 16, base + voff[i], 0, 0,
-                                               0);
+      for (int i = 0; i < LOADS; i++) {
+        const int dst = (wave * LOADS + i) * KPI * RB;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_ptr_t)(smem + (2 + buf) * TILE + dst), 16, base + voff[i],
+                                                 0, 0, 0);
+      }
     }
   };
 
@@ -182,49 +196,59 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_bf16(AttnArgs a) {
   float m_run = -INFINITY, l_run = 0.f;
 
   const int nt = cdiv(S, KB);
-  issue(0, 0);
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  for (int kt = 0; kt < nt; kt++) {
-    const int buf = kt & 1;
-    if (kt + 1 < nt) issue(kt + 1, buf ^ 1);   // buf^1 was last read before the previous barrier
-    const char* sk = smem + buf * TILE;
-    const char* sv = smem + (2 + buf) * TILE;
-
-    // S^T blocks: keys 32 kb + 8(r/4) + 4 half + r%4 of this lane's query. All K fragments of the
-    // tile are requested before the first score MFMA (pinned by the scheduling groups below; left to
-    // itself the compiler reused one register pair per step and waited on every read), so only the
-    // first MFMA waits for LDS.
-    f32x16 st[KB / 32];
-    bf16x8 kf[NKS][KB / 32];
+  // S^T blocks of a tile: keys 32 kb + 8(r/4) + 4 half + r%4 of this lane's query. The head dims are
+  // taken in four groups; a group's K fragments are read just before its MFMAs.
+  auto scores = [&](int kt, f32x16* sn) {
+    const char* sk = smem + (kt & 1) * TILE;
+    constexpr int NS = NKS / 4 > 0 ? NKS / 4 : 1;
 #pragma unroll
-    for (int s = 0; s < NKS; s++)
+    for (int g = 0; g < NKS / NS; g++) {
+      bf16x8 kf[NS][KB / 32];
 #pragma unroll
-      for (int kb = 0; kb < KB / 32; kb++)
-        kf[s][kb] = *(const bf16x8*)(sk + 32 * kb * RB + krow + (((2 * s + half) ^ ksw) << 4));
+      for (int s = 0; s < NS; s++)
 #pragma unroll
-    for (int s = 0; s < NKS; s++)
+        for (int kb = 0; kb < KB / 32; kb++)
+          kf[s][kb] = *(const bf16x8*)(sk + 32 * kb * RB + krow + (((2 * (g * NS + s) + half) ^ ksw) << 4));
 #pragma unroll
-      for (int kb = 0; kb < KB / 32; kb++)
-        st[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s][kb], qf[s], s == 0 ? zero : st[kb], 0, 0, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, NKS * (KB / 32), 0);   // the K fragment reads
-    __builtin_amdgcn_sched_group_barrier(0x008, NKS * (KB / 32), 0);   // then the score MFMAs
-    __builtin_amdgcn_sched_barrier(0);
-    // mask keys past the end (last tile only)
+      for (int s = 0; s < NS; s++)
+#pragma unroll
+        for (int kb = 0; kb < KB / 32; kb++) {
+          const int sg = g * NS + s;
+          sn[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s][kb], qf[sg], sg == 0 ? zero : sn[kb], 0, 0, 0);
+        }
+    }
+  };
+  // keys past the end of the sequence (last tile only) score -inf; returns this lane's max
+  auto mask_max = [&](int kt, f32x16* sn) {
     if ((kt + 1) * KB > S) {
 #pragma unroll
       for (int kb = 0; kb < KB / 32; kb++)
 #pragma unroll
         for (int r = 0; r < 16; r++) {
           int key = kt * KB + 32 * kb + 8 * (r >> 2) + 4 * half + (r & 3);
-          if (key >= S) st[kb][r] = -INFINITY;
+          if (key >= S) sn[kb][r] = -INFINITY;
         }
     }
     float mx = -INFINITY;
 #pragma unroll
     for (int kb = 0; kb < KB / 32; kb++)
 #pragma unroll
-      for (int r = 0; r < 16; r++) mx = fmaxf(mx, st[kb][r]);
+      for (int r = 0; r < 16; r++) mx = fmaxf(mx, sn[kb][r]);
+    return mx;
+  };
+
+  // One step of the software pipeline. On entry st holds the scores of tile kt and mx their lane max.
+  // The exponentials of tile kt and the score MFMAs of tile kt+1 (NEXT) sit in one instruction stream,
+  // so the compiler can issue the one between the other; then tile kt's P V^T runs. K tiles are
+  // requested two tiles ahead and V tiles one ahead, each in its own pair of LDS buffers.
+  auto step = [&](int kt, f32x16* st, float& mx, f32x16* sn, float& mxn, auto next_c) {
+    constexpr bool NEXT = decltype(next_c)::value;
+    // every wave is done with K buffer kt&1 (scores of kt, in the previous step) and V buffer
+    // (kt+1)&1 (P V^T of kt-1); this wave's loads into the buffers read below have landed
+    __syncthreads();
+    if (kt + 2 < nt) issue_k(kt + 2, kt & 1);
+    if (NEXT) issue_v(kt + 1, (kt + 1) & 1);
+    const char* sv = smem + (2 + (kt & 1)) * TILE;
     mx = pair_max(mx);   // with the other 16 keys of each 32-key block (lane ^ 32)
     const float mxs = mx * c;
     if (__ballot(mxs > m_run + TAU) != 0) {   // some row's max moved by more than TAU
@@ -249,32 +273,49 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_bf16(AttnArgs a) {
           psum += p;
           pf[kb][t][j] = (__bf16)p;
         }
+    if constexpr (NEXT) scores(kt + 1, sn);
     l_run += psum;
 
-    // O^T[dim][query] += V^T[dim][keys] P^T[keys][query] over the KB/16 key steps; the V^T
-    // fragments of step q+1 are read during step q. Step q covers keys 16 q + {4 half + 0..3,
-    // 8 + 4 half + 0..3}, the order of the score accumulator.
-    bf16x8 vfr[2][NDB];
-    auto read_v = [&](int q, int slot) {
+    // O^T[dim][query] += V^T[dim][keys] P^T[keys][query] over the KB/16 key steps. Step q covers
+    // keys 16 q + {4 half + 0..3, 8 + 4 half + 0..3}, the order of the score accumulator.
+#pragma unroll
+    for (int q = 0; q < KB / 16; q++) {
+      bf16x8 vfr[NDB];
 #pragma unroll
       for (int db = 0; db < NDB; db++) {
         const char* p0 = sv + 16 * q * RB + vbase[db];
         i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(p0));
         i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(p0 + 8 * RB));
-        i16x8 w = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-        vfr[slot][db] = __builtin_bit_cast(bf16x8, w);
+        vfr[db] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
       }
-    };
-    read_v(0, 0);
-#pragma unroll
-    for (int q = 0; q < KB / 16; q++) {
-      if (q + 1 < KB / 16) read_v(q + 1, (q + 1) & 1);
 #pragma unroll
       for (int db = 0; db < NDB; db++)
-        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vfr[q & 1][db], pf[q >> 1][q & 1], o[db], 0, 0, 0);
+        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vfr[db], pf[q >> 1][q & 1], o[db], 0, 0, 0);
     }
-    __builtin_amdgcn_s_waitcnt(0);   // this wave's share of tile kt+1 landed; its reads of buf are done
-    __syncthreads();                 // ... in every wave
+    if constexpr (NEXT) mxn = mask_max(kt + 1, sn);
+    __builtin_amdgcn_s_waitcnt(0);   // this wave's loads of K(kt+2) and V(kt+1) landed
+  };
+
+  issue_k(0, 0);
+  issue_v(0, 0);
+  if (nt > 1) issue_k(1, 1);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  // two score buffers, used alternately (the loop is unrolled by two so that neither is copied)
+  f32x16 sa[KB / 32], sb[KB / 32];
+  float ma, mb = -INFINITY;
+  scores(0, sa);
+  ma = mask_max(0, sa);
+  int kt = 0;
+  for (; kt + 2 < nt; kt += 2) {
+    step(kt, sa, ma, sb, mb, std::true_type());
+    step(kt + 1, sb, mb, sa, ma, std::true_type());
+  }
+  if (kt + 1 < nt) {
+    step(kt, sa, ma, sb, mb, std::true_type());
+    step(kt + 1, sb, mb, sa, ma, std::false_type());
+  } else {
+    step(kt, sa, ma, sb, mb, std::false_type());
   }
 
   // normalise: full row sum = this lane's part + lane^32's part
