@@ -3,7 +3,10 @@
     python -m paper_2606_19004_amd.build        # or build() from Python
 
 Each .hip (and host-only .cpp) under csrc/ compiles to an object under _build/ (in parallel), then
-the objects link into paper_2606_19004_amd/libditstep.so.
+the objects link into paper_2606_19004_amd/libditstep.so. The same objects with api.hip compiled under
+DITSTEP_DEBUG link into libditstep_debug.so: every launch synchronised and checked, and every operand
+range of the block path's GEMM, attention and LayerNorm launches checked against the buffers the
+entry point knows.
 """
 from __future__ import annotations
 
@@ -18,6 +21,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 OBJ = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libditstep.so")
+LIB_DEBUG = os.path.join(HERE, "libditstep_debug.so")
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [
@@ -54,6 +58,8 @@ def build(verbose: bool = False, jobs: int = 4) -> str:
     objs = [os.path.join(OBJ, f.rsplit(".", 1)[0] + ".o") for f in srcs]
     cmds = [[cc, *(HIPCC_FLAGS if f.endswith(".hip") else HOST_FLAGS), "-c", os.path.join(CSRC, f), "-o", o]
             for f, o in zip(srcs, objs)]
+    api_debug = os.path.join(OBJ, "api_debug.o")
+    cmds.append([cc, *HIPCC_FLAGS, "-DDITSTEP_DEBUG", "-c", os.path.join(CSRC, "api.hip"), "-o", api_debug])
     with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
         results = list(ex.map(_run, cmds))
     for cmd, (rc, out) in zip(cmds, results):
@@ -61,12 +67,13 @@ def build(verbose: bool = False, jobs: int = 4) -> str:
             print(out)
         if rc != 0:
             raise RuntimeError(f"hipcc failed ({rc}) for {cmd[-3]}:\n{out}")
-    tmp = LIB + ".tmp"
-    rc, out = _run([cc, "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp,
-                    *objs])
-    if rc != 0:
-        raise RuntimeError(f"link failed:\n{out}")
-    os.replace(tmp, LIB)
+    debug_objs = [api_debug if os.path.basename(o) == "api.o" else o for o in objs]
+    for lib, lib_objs in ((LIB, objs), (LIB_DEBUG, debug_objs)):
+        tmp = lib + ".tmp"
+        rc, out = _run([cc, "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp, *lib_objs])
+        if rc != 0:
+            raise RuntimeError(f"link failed:\n{out}")
+        os.replace(tmp, lib)
     return LIB
 
 

@@ -4,6 +4,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <atomic>
+#include <cstdlib>
 #include <cstring>
 #include <limits>
 #include <map>
@@ -42,8 +43,28 @@ Prof g_prof;
 // set while an allocation-free entry point runs on this thread: no timing events are created
 thread_local bool g_no_events = false;
 
+#ifdef DITSTEP_DEBUG
+// Debug builds: every launch is followed by a synchronisation of its stream (unless the stream is
+// being captured) and a check of the launch and of the kernel's completion.
 template <class F>
-hipError_t timed(const char* name, double flops, double bytes, hipStream_t s, F&& launch) {
+hipError_t checked(hipStream_t s, F&& launch) {
+  hipError_t e = launch();
+  if (e != hipSuccess) return e;
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  if ((e = hipStreamIsCapturing(s, &cs)) != hipSuccess) return e;
+  if (cs != hipStreamCaptureStatusNone) return hipSuccess;
+  if ((e = hipStreamSynchronize(s)) != hipSuccess) return e;
+  return hipGetLastError();
+}
+#endif
+
+template <class F>
+hipError_t timed(const char* name, double flops, double bytes, hipStream_t s, F&& launch_) {
+#ifdef DITSTEP_DEBUG
+  auto launch = [&]() { return checked(s, launch_); };
+#else
+  auto& launch = launch_;
+#endif
   if (g_no_events || !g_prof.on.load(std::memory_order_acquire)) return launch();
   hipEvent_t a, b;
   hipError_t e = hipEventCreate(&a);
@@ -200,6 +221,115 @@ dit_status run_modulation_group(const dit_block_config* c, const dit_block_weigh
 }
 
 // h = LN(x)(1+scale)+shift for both streams into the joint [B][S][D] buffer
+#ifdef DITSTEP_DEBUG
+// Debug builds: the entry points of the block path register the buffers whose sizes they know (the
+// workspace, the residual streams, the modulation, the block's weights), and every operand range a
+// GEMM, attention or LayerNorm launch addresses must lie inside one of them.
+struct DbgRegions {
+  const char* base[32];
+  size_t bytes[32];
+  int n = 0;
+  void add(const void* p, size_t b) {
+    if (p && n < 32) {
+      base[n] = (const char*)p;
+      bytes[n] = b;
+      n++;
+    }
+  }
+  bool holds(const void* p, size_t b) const {
+    const char* q = (const char*)p;
+    for (int i = 0; i < n; i++)
+      if (q >= base[i] && q + b <= base[i] + bytes[i]) return true;
+    return false;
+  }
+};
+thread_local const DbgRegions* g_dbg = nullptr;
+struct DbgScope {
+  const DbgRegions* prev;
+  explicit DbgScope(const DbgRegions* r) : prev(g_dbg) { g_dbg = r; }
+  ~DbgScope() { g_dbg = prev; }
+};
+// one past the largest element a row map addresses for rows x cols (row maps grow with the row)
+size_t map_extent(const RowMap& m, int64_t rows, int64_t cols) {
+  return rows <= 0 ? 0 : (size_t)(row_offset(m, rows - 1) + cols);
+}
+DbgRegions block_regions(const dit_block_config* c, const dit_block_weights* w, int B, const void* x_img,
+                         const void* x_txt, const char* ws, size_t ws_bytes, const float* mod) {
+  DbgRegions r;
+  const size_t es = esize(c->dtype), D = c->hidden, F = c->mlp_hidden;
+  // test hook: register the workspace 4 KB short, so that the checks must refuse the launches
+  // whose operands reach its end (the MLP hidden buffer is its last region)
+  if (std::getenv("DITSTEP_DEBUG_SHRINK_WS") && ws_bytes > 4096) ws_bytes -= 4096;
+  r.add(ws, ws_bytes);
+  r.add(x_img, (size_t)B * c->n_img * D * es);
+  r.add(x_txt, (size_t)B * c->n_txt * D * es);
+  r.add(mod, (size_t)2 * B * 6 * D * 4);
+  for (int i = 0; i < 2; i++) {
+    r.add(w->mod_w[i], 6 * D * D * es);
+    r.add(w->mod_b[i], 6 * D * es);
+    r.add(w->qkv_w[i], 3 * D * D * es);
+    r.add(w->qkv_b[i], 3 * D * es);
+    r.add(w->out_w[i], D * D * es);
+    r.add(w->out_b[i], D * es);
+    r.add(w->mlp1_w[i], F * D * es);
+    r.add(w->mlp1_b[i], F * es);
+    r.add(w->mlp2_w[i], D * F * es);
+    r.add(w->mlp2_b[i], D * es);
+  }
+  return r;
+}
+dit_status dbg_fail(const char* what, const char* operand, int i) {
+  return set_error(DIT_ERR_INVALID_ARG, "debug check: %s launch, problem %d: %s outside every known buffer", what,
+                   i, operand);
+}
+dit_status dbg_gemm(const GemmPair& pr, size_t es, const char* what) {
+  if (!g_dbg) return DIT_OK;
+  for (int i = 0; i < pr.nprob; i++) {
+    const GemmProblem& p = pr.p[i];
+    if (p.M <= 0 || p.N <= 0) continue;
+    if (!g_dbg->holds(p.A, map_extent(p.amap, p.M, p.K) * es)) return dbg_fail(what, "A", i);
+    if (!g_dbg->holds(p.W, (size_t)p.N * p.K * es)) return dbg_fail(what, "W", i);
+    if (p.bias && !g_dbg->holds(p.bias, (size_t)p.N * es)) return dbg_fail(what, "bias", i);
+    if (!g_dbg->holds(p.C, map_extent(p.cmap, p.M, p.N) * es)) return dbg_fail(what, "C", i);
+    if (p.gate) {
+      const int64_t nb = (p.M - 1) / p.cmap.rows_per_batch + 1;
+      if (!g_dbg->holds(p.gate, (size_t)((nb - 1) * p.gate_bstride + p.N) * 4)) return dbg_fail(what, "gate", i);
+    }
+  }
+  return DIT_OK;
+}
+dit_status dbg_attn(const AttnArgs& a, size_t es) {
+  if (!g_dbg) return DIT_OK;
+  const size_t in = (size_t)((a.B - 1) * a.qs_b + (a.S - 1) * a.qs_s + (a.H - 1) * a.qs_h + a.d) * es;
+  const size_t out = (size_t)((a.B - 1) * a.os_b + (a.S - 1) * a.os_s + (a.H - 1) * a.os_h + a.d) * es;
+  if (!g_dbg->holds(a.q, in)) return dbg_fail("attention", "q", 0);
+  if (!g_dbg->holds(a.k, in)) return dbg_fail("attention", "k", 0);
+  if (!g_dbg->holds(a.v, in)) return dbg_fail("attention", "v", 0);
+  if (!g_dbg->holds(a.o, out)) return dbg_fail("attention", "o", 0);
+  return DIT_OK;
+}
+dit_status dbg_ln(const LnArgs& a, size_t es) {
+  if (!g_dbg) return DIT_OK;
+  for (int i = 0; i < 2; i++) {
+    if (a.rows[i] <= 0) continue;
+    if (!g_dbg->holds(a.x[i], map_extent(a.xmap[i], a.rows[i], a.D) * es)) return dbg_fail("ln_modulate", "x", i);
+    if (!g_dbg->holds(a.out, map_extent(a.omap[i], a.rows[i], a.D) * es)) return dbg_fail("ln_modulate", "out", i);
+    const int64_t nb = (a.rows[i] - 1) / a.xmap[i].rows_per_batch + 1;
+    const size_t mod = (size_t)((nb - 1) * a.mod_bstride + std::max(a.shift_off, a.scale_off) + a.D) * 4;
+    if (!g_dbg->holds(a.mod[i], mod)) return dbg_fail("ln_modulate", "mod", i);
+  }
+  return DIT_OK;
+}
+#define DBG_CHECK(expr)                      \
+  do {                                       \
+    if (dit_status d_ = (expr)) return d_;   \
+  } while (0)
+#else
+#define DBG_CHECK(expr) \
+  do {                  \
+  } while (0)
+#endif
+
 dit_status run_ln(const dit_block_config* c, int B, const void* x_img, const void* x_txt, const float* mod,
                   char* ws, const BlockWs& L, int shift_off, int scale_off, hipStream_t s) {
   const int D = c->hidden;
@@ -220,6 +350,7 @@ dit_status run_ln(const dit_block_config* c, int B, const void* x_img, const voi
   a.rows[1] = (int64_t)B * c->n_txt;
   a.D = D;
   a.eps = c->ln_eps;
+  DBG_CHECK(dbg_ln(a, esize(c->dtype)));
   TIMED("ln_modulate", 0, 2.0 * (a.rows[0] + a.rows[1]) * D * esize(c->dtype), s, ln_modulate(a, c->dtype, s));
   return DIT_OK;
 }
@@ -257,6 +388,8 @@ dit_status run_mlp_half(const dit_block_config* c, const dit_block_weights* w, i
     down.p[i].gate = mod + (size_t)i * B * 6 * D + 5 * D;
     down.p[i].gate_bstride = 6 * D;
   }
+  DBG_CHECK(dbg_gemm(up, esize(c->dtype), "gemm_mlp_up_gelu"));
+  DBG_CHECK(dbg_gemm(down, esize(c->dtype), "gemm_mlp_down_gate"));
   TIMED("gemm_mlp_up_gelu", gemm_flops(up), 0, s, gemm(up, EPI_GELU, c->dtype, false, s));
   TIMED("gemm_mlp_down_gate", gemm_flops(down), 0, s, gemm(down, EPI_RESID, c->dtype, false, s));
   return DIT_OK;
@@ -446,6 +579,10 @@ dit_status block_body(const dit_block_config* c, const dit_block_weights* w, int
   const int64_t nstream[2] = {c->n_img, c->n_txt};
   const float* mod = mod_pre ? mod_pre : (const float*)(ws + L.mod);
   float* rope = (float*)(ws + L.rope);
+#ifdef DITSTEP_DEBUG
+  const DbgRegions dbg_r = block_regions(c, w, B, x_img, x_txt, ws, L.total, mod);
+  const DbgScope dbg_scope(&dbg_r);
+#endif
 
   if (!mod_pre && (st = run_modulation(c, w, B, temb, ws, L, s))) return st;
   if (c->rope && !rope_ready)
@@ -466,6 +603,7 @@ dit_status block_body(const dit_block_config* c, const dit_block_weights* w, int
     qkv.p[0].rope_tab = rope;
     qkv.p[0].rope_npos = std::max(c->grid_h, c->grid_w);
   }
+  DBG_CHECK(dbg_gemm(qkv, esize(c->dtype), "gemm_qkv_rope"));
   TIMED("gemm_qkv_rope", gemm_flops(qkv), 0, s, gemm(qkv, EPI_QKV, c->dtype, false, s));
   // joint attention over [text ; image]; output o reuses the h buffer
   AttnArgs at{};
@@ -486,6 +624,7 @@ dit_status block_body(const dit_block_config* c, const dit_block_weights* w, int
   at.os_s = D;
   at.os_h = d;
   at.scale = 1.0f / std::sqrt((float)d);
+  DBG_CHECK(dbg_attn(at, esize(c->dtype)));
   TIMED("attention", 4.0 * B * H * (double)S * S * d, 0, s, attention(at, c->dtype, s));
   // output projection + gate1 residual, in place on x
   GemmPair proj{};
@@ -496,6 +635,7 @@ dit_status block_body(const dit_block_config* c, const dit_block_weights* w, int
     proj.p[i].gate = mod + (size_t)i * B * 6 * D + 2 * D;
     proj.p[i].gate_bstride = 6 * D;
   }
+  DBG_CHECK(dbg_gemm(proj, esize(c->dtype), "gemm_out_gate"));
   TIMED("gemm_out_gate", gemm_flops(proj), 0, s, gemm(proj, EPI_RESID, c->dtype, false, s));
   return run_mlp_half(c, w, B, x_img, x_txt, mod, ws, L, s);
 }
@@ -538,6 +678,10 @@ dit_status dit_block_mlp(const dit_block_config* c, const dit_block_weights* w, 
   if ((st = check_ws(workspace, workspace_bytes, L.total))) return st;
   char* ws = (char*)workspace;
   if ((st = run_modulation(c, w, batch, temb, ws, L, hs(stream)))) return st;
+#ifdef DITSTEP_DEBUG
+  const DbgRegions dbg_r = block_regions(c, w, batch, x_img, x_txt, ws, L.total, (const float*)(ws + L.mod));
+  const DbgScope dbg_scope(&dbg_r);
+#endif
   return run_mlp_half(c, w, batch, x_img, x_txt, (const float*)(ws + L.mod), ws, L, hs(stream));
 }
 

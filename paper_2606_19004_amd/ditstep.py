@@ -16,7 +16,8 @@ import os
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libditstep.so")
+# DITSTEP_LIB selects another build of the library (the DITSTEP_DEBUG build, libditstep_debug.so)
+LIB_PATH = os.environ.get("DITSTEP_LIB") or os.path.join(_HERE, "libditstep.so")
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2606_19004_amd.build`")
