@@ -247,7 +247,6 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_bf16(AttnArgs a) {
     // (kt+1)&1 (P V^T of kt-1); this wave's loads into the buffers read below have landed
     __syncthreads();
     if (kt + 2 < nt) issue_k(kt + 2, kt & 1);
-    if (NEXT) issue_v(kt + 1, (kt + 1) & 1);
     const char* sv = smem + (2 + (kt & 1)) * TILE;
     mx = pair_max(mx);   // with the other 16 keys of each 32-key block (lane ^ 32)
     const float mxs = mx * c;
@@ -275,6 +274,10 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_bf16(AttnArgs a) {
         }
     if constexpr (NEXT) scores(kt + 1, sn);
     l_run += psum;
+    // V(kt+1) is requested only now: issued together with K(kt+2) right after the barrier, the
+    // eight waves' loads queued behind each other for ~650 cycles per step; here they meet
+    // fewer, and still land before the step's final wait
+    if (NEXT) issue_v(kt + 1, (kt + 1) & 1);
 
     // O^T[dim][query] += V^T[dim][keys] P^T[keys][query] over the KB/16 key steps. Step q covers
     // keys 16 q + {4 half + 0..3, 8 + 4 half + 0..3}, the order of the score accumulator.
