@@ -31,6 +31,10 @@
 //     when a row's new max exceeds it by more than TAU in the exp2 domain, so
 //     probabilities stay below 2^TAU; the normalisation divides by a row sum taken
 //     against the same max, so the result is unchanged.
+//   * The normalised output leaves through LDS (the K buffers, free after the last
+//     step): a wave writes its 32 rows in the accumulator layout and stores them
+//     back as whole rows, one 16-byte chunk per lane, instead of 8-byte pieces
+//     scattered over 32 rows per store.
 //   * Workgroups are dispatched round-robin over the 8 XCDs; each XCD gets a
 //     contiguous range of (sample, head, query block) tiles, so the query blocks
 //     of one (sample, head) read its K/V through the same L2.
@@ -324,18 +328,32 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_bf16(AttnArgs a) {
   // normalise: full row sum = this lane's part + lane^32's part
   float l_all = pair_sum(l_run);
   const float inv = 1.0f / l_all;
-  if (qi < S) {
-    u16* orow = (u16*)a.o + (int64_t)b * a.os_b + (int64_t)qi * a.os_s + (int64_t)h * a.os_h;
+  // The output tile goes out through LDS: both K buffers are free once every wave has passed the last
+  // step's barrier (the last K tile was read by the step before), and each wave uses the 32 rows of
+  // that area that hold its own queries, so no further barrier is needed. A wave writes its rows in
+  // the accumulator layout (16-byte chunk c of row r at slot c ^ (r mod CH)) and reads them back as
+  // whole rows, so that every global store writes complete output rows.
+  {
+    char* so = smem + wave * 32 * RB;
 #pragma unroll
     for (int db = 0; db < NDB; db++)
 #pragma unroll
       for (int g = 0; g < 4; g++) {
-        int dim = 32 * db + 8 * g + 4 * half;
+        const int c = 4 * db + g;
         uint2 u;
         u.x = (uint32_t)from_f32<u16>(o[db][4 * g] * inv) | ((uint32_t)from_f32<u16>(o[db][4 * g + 1] * inv) << 16);
         u.y = (uint32_t)from_f32<u16>(o[db][4 * g + 2] * inv) | ((uint32_t)from_f32<u16>(o[db][4 * g + 3] * inv) << 16);
-        *(uint2*)(orow + dim) = u;
+        *(uint2*)(so + l32 * RB + ((c ^ (l32 % CH)) << 4) + 8 * half) = u;
       }
+    constexpr int RPI = 64 / CH;   // rows per wave store (CH lanes of 16 bytes per row)
+    u16* obase = (u16*)a.o + (int64_t)b * a.os_b + (int64_t)h * a.os_h;
+#pragma unroll
+    for (int i = 0; i < 32 / RPI; i++) {
+      const int r = i * RPI + lane / CH, c = lane % CH;
+      const uint4 v = *(const uint4*)(so + r * RB + ((c ^ (r % CH)) << 4));
+      const int q = qblk * QB + wave * 32 + r;
+      if (q < S) *(uint4*)(obase + (int64_t)q * a.os_s + 8 * c) = v;
+    }
   }
 #endif
 }
