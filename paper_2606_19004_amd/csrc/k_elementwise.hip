@@ -485,8 +485,13 @@ __global__ void split_hilo_kernel(const float* __restrict__ in, int64_t stride, 
 // workgroup mean fewer re-reads of the input per weight byte: with the weights cold in HBM, RB = 8
 // (one k step per wave in flight, 180 registers) streams the 1.81 GB of a step's modulation
 // weights in 426 us against 467 us for RB = 4 with two k steps in flight. Small GEMVs (the
-// timestep and final-layer ones) keep RB = 4, which gives twice the workgroups to fill the chip.
-template <int RB, int U>
+// timestep and final-layer ones, a few MB of weights) are bound by the latency of each wave's chain
+// of k steps instead: they take fewer rows per workgroup (more workgroups) and, with DEPTH > 0, keep
+// DEPTH of a wave's k steps in flight (the loads of step i + DEPTH - 1 are issued before the MFMAs
+// of step i; loads past the wave's last step are clamped to that step, so that every load is
+// unconditional and the compiler can count the loads in flight). The sums run in the same order
+// either way.
+template <int RB, int U, int DEPTH = 0>
 __global__ void __launch_bounds__(256) gemv_mfma_kernel(GemvArgs a, const u16* __restrict__ xs, int b0, int nb) {
   __shared__ f32x4 part[4][RB][64];
   const int s = blockIdx.y;
@@ -505,33 +510,72 @@ __global__ void __launch_bounds__(256) gemv_mfma_kernel(GemvArgs a, const u16* _
   f32x4 acc[RB];
 #pragma unroll
   for (int j = 0; j < RB; j++) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-  int ks = wave;
-  for (; ks + 4 * (U - 1) < nks; ks += 4 * U) {
-    bf16x8 fw[U][RB], fh[U], fl[U];
+  if constexpr (DEPTH == 0) {
+    int ks = wave;
+    for (; ks + 4 * (U - 1) < nks; ks += 4 * U) {
+      bf16x8 fw[U][RB], fh[U], fl[U];
 #pragma unroll
-    for (int u = 0; u < U; u++) {
-      int k = 32 * (ks + 4 * u);
+      for (int u = 0; u < U; u++) {
+        int k = 32 * (ks + 4 * u);
 #pragma unroll
-      for (int j = 0; j < RB; j++) fw[u][j] = *(const bf16x8*)(w[j] + k);
-      fh[u] = *(const bf16x8*)(xh + k);
-      fl[u] = *(const bf16x8*)(xl + k);
+        for (int j = 0; j < RB; j++) fw[u][j] = *(const bf16x8*)(w[j] + k);
+        fh[u] = *(const bf16x8*)(xh + k);
+        fl[u] = *(const bf16x8*)(xl + k);
+      }
+#pragma unroll
+      for (int u = 0; u < U; u++)
+#pragma unroll
+        for (int j = 0; j < RB; j++) {
+          acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fw[u][j], fh[u], acc[j], 0, 0, 0);
+          acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fw[u][j], fl[u], acc[j], 0, 0, 0);
+        }
     }
-#pragma unroll
-    for (int u = 0; u < U; u++)
+    for (; ks < nks; ks += 4) {
+      int k = 32 * ks;
+      bf16x8 fh = *(const bf16x8*)(xh + k), fl = *(const bf16x8*)(xl + k);
 #pragma unroll
       for (int j = 0; j < RB; j++) {
-        acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fw[u][j], fh[u], acc[j], 0, 0, 0);
-        acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fw[u][j], fl[u], acc[j], 0, 0, 0);
+        bf16x8 fw = *(const bf16x8*)(w[j] + k);
+        acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fw, fh, acc[j], 0, 0, 0);
+        acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fw, fl, acc[j], 0, 0, 0);
       }
-  }
-  for (; ks < nks; ks += 4) {
-    int k = 32 * ks;
-    bf16x8 fh = *(const bf16x8*)(xh + k), fl = *(const bf16x8*)(xl + k);
+    }
+  } else {
+    // this wave's k steps are wave + 4 i, i < nloc; the first nmain of them run pipelined
+    const int nloc = nks > wave ? (nks - wave + 3) / 4 : 0;
+    const int nmain = nloc - nloc % DEPTH;
+    bf16x8 fw[DEPTH][RB], fh[DEPTH], fl[DEPTH];
+    auto load = [&](int i, int slot) {
+      const int k = 32 * (wave + 4 * i);
 #pragma unroll
-    for (int j = 0; j < RB; j++) {
-      bf16x8 fw = *(const bf16x8*)(w[j] + k);
-      acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fw, fh, acc[j], 0, 0, 0);
-      acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fw, fl, acc[j], 0, 0, 0);
+      for (int j = 0; j < RB; j++) fw[slot][j] = *(const bf16x8*)(w[j] + k);
+      fh[slot] = *(const bf16x8*)(xh + k);
+      fl[slot] = *(const bf16x8*)(xl + k);
+    };
+    auto mma = [&](int slot) {
+#pragma unroll
+      for (int j = 0; j < RB; j++) {
+        acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fw[slot][j], fh[slot], acc[j], 0, 0, 0);
+        acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fw[slot][j], fl[slot], acc[j], 0, 0, 0);
+      }
+    };
+    if (nmain > 0) {
+#pragma unroll
+      for (int d = 0; d < DEPTH - 1; d++) load(d, d);
+      __builtin_amdgcn_sched_barrier(0);
+      for (int i = 0; i < nmain; i += DEPTH) {
+#pragma unroll
+        for (int u = 0; u < DEPTH; u++) {
+          load(min(i + u + DEPTH - 1, nloc - 1), (u + DEPTH - 1) % DEPTH);
+          __builtin_amdgcn_sched_barrier(0);   // keep the loads ahead of this step's MFMAs
+          mma(u);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+    }
+    for (int i = nmain; i < nloc; i++) {
+      load(i, 0);
+      mma(0);
     }
   }
 #pragma unroll
@@ -566,10 +610,19 @@ hipError_t gemv_bf16(const GemvArgs& a, u16* xs, int silu_in, hipStream_t s) {
   for (int b0 = 0; b0 < a.B; b0 += 16) {
     int nb = std::min(16, a.B - b0);
     split_hilo_kernel<<<dim3(cdiv(a.K, 256), 16), 256, 0, s>>>(a.in, a.in_bstride, b0, nb, a.K, silu_in, xs);
-    if ((int64_t)cdiv(a.N, 128) * a.nstreams >= 1024)
+    // rows per workgroup by grid size: the step's batched modulation (1.8 GB of weights) streams
+    // best with 128; a single block's (0.2 GB) with 64; the timestep and final-layer GEMVs (a few
+    // MB) need more workgroups and a pipelined k chain (lab, same box: 30 -> 18 us for 3072 x 3072,
+    // 31 -> 20 us for 6144 x 3072, bit-identical)
+    const int64_t ns = a.nstreams;
+    if ((int64_t)cdiv(a.N, 128) * ns >= 1024)
       gemv_mfma_kernel<8, 1><<<dim3(cdiv(a.N, 128), a.nstreams), 256, 0, s>>>(a, xs, b0, nb);
-    else
+    else if ((int64_t)cdiv(a.N, 64) * ns >= 256)
       gemv_mfma_kernel<4, 2><<<dim3(cdiv(a.N, 64), a.nstreams), 256, 0, s>>>(a, xs, b0, nb);
+    else if ((int64_t)cdiv(a.N, 32) * ns >= 192)
+      gemv_mfma_kernel<2, 1, 2><<<dim3(cdiv(a.N, 32), a.nstreams), 256, 0, s>>>(a, xs, b0, nb);
+    else
+      gemv_mfma_kernel<1, 1, 4><<<dim3(cdiv(a.N, 16), a.nstreams), 256, 0, s>>>(a, xs, b0, nb);
   }
   return hipGetLastError();
 }
