@@ -1,7 +1,7 @@
 """The library's host-only code (the exploration planner and seed bank, argument validation, flow
 coefficients, the TeaCache gate and the error text) built with g++ under AddressSanitizer and
 UndefinedBehaviorSanitizer, driven through valid, boundary and invalid calls by
-tests/host_sanitize/driver.cpp. No GPU; the device code is not part of this build."""
+tests/host_sanitize/driver.cpp. No GPU; the device code is not compiled for it."""
 import os
 import shutil
 import subprocess
