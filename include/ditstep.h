@@ -28,9 +28,11 @@
  *     fp32 epilogue math; DIT_F32 = fp32 throughout. temb, the latent, the
  *     velocity, noise and rewards are always fp32.
  *   - Thread safety: no mutable global state besides the per-thread error
- *     text and per-device caches filled once (atomics: the device's compute
- *     unit count and the kernels' LDS limits); calls on different streams
- *     with disjoint buffers may overlap, also on their first call.
+ *     text, per-device caches filled once (atomics: the device's compute
+ *     unit count and the kernels' LDS limits) and the fixed scratch array of
+ *     dit_timestep_embed_noalloc (one per GPU; overlapping calls of that entry
+ *     point on one GPU race); calls on different streams with disjoint
+ *     buffers may overlap, also on their first call.
  */
 #ifndef DITSTEP_H
 #define DITSTEP_H
