@@ -439,6 +439,26 @@ def make_step(d, cfg, x):
     return step
 
 
+def graph_replay(torch, step, steps, warmup):
+    """The same step (denoise step and reward statistics) captured once into a HIP graph and
+    replayed: wall clock per replay over `steps` replays. The step records only kernels and one
+    device-to-device copy, so the graph replays it as launched."""
+    g = torch.cuda.CUDAGraph()
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        step()
+    for _ in range(max(warmup, 1)):
+        g.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        g.replay()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    del g
+    return {"ms_per_step": round(ms, 4), "steps": steps}
+
+
 def next_rows(torch, d, cfg, x):
     """Rows past the denoise step: the SDE step's log-density on this workload's latents (GPU,
     timed with HIP events over 20 launches), and one planner iteration plus the seed-bank update
@@ -701,8 +721,9 @@ def main():
     summary["attention_frac"] = (round(summary["attention_tflops"] / PEAK_BF16_TFLOPS, 4)
                                  if summary["attention_tflops"] else None)
 
-    extra = blocks = None
+    extra = blocks = graph = None
     if not args.headline_only:
+        graph = graph_replay(torch, step, args.steps, args.warmup)
         extra = next_rows(torch, d, cfg, x)
         del x, step
         torch.cuda.empty_cache()
@@ -724,6 +745,7 @@ def main():
                    "batch": cfg.batch, "seq_len": cfg.seq, "blocks": cfg.blocks, "parallelism": "single GPU"},
         "roofline": roofline,
         "mfma_summary": summary,
+        "graph_replay": graph,
         "kernels": kernels,
         "next_rows": extra,
         "other_configs": blocks,
